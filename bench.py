@@ -1,0 +1,337 @@
+#!/usr/bin/env python3
+"""Benchmark of the block-sparse attention forward on one MI355X.
+
+A step is one call of ``sa_bsattn_fwd`` (mask pre-pass, schedule and the
+attention kernel) on resident inputs of the Wan2.1-14B-like 480p shape
+(B=1, H=40, N=32768, d=128, 128 x 128 blocks, structured per-head masks with
+density U[0.05, 0.6]).  The metric is effective TFLOP/s: 4 * 128 * 128 * 128
+flops per executed (enabled) block divided by the step time.
+
+Printed (one JSON line on stdout): the metric, the fraction of the bf16 MFMA
+peak, speedup over the same kernel with an all-ones mask, a roofline record
+for the attention kernel (timed with events on the stream it runs on) and the
+CPU reference timed on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--workload 14b-480p]
+  python bench.py --sweep out.json     # density / block sweep, extra file
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "attn_fwd_14b480p_hbm_traffic.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_23019_amd", "csrc", "attn_fwd.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def flops_per_block(wl):
+    return 4.0 * wl.blk_q * wl.blk_k * wl.d
+
+
+def _events_time(fn, steps):
+    """Run fn() ``steps`` times between two events on the current stream; ms per call."""
+    import torch
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(steps):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps
+
+
+def _per_launch_time(fn, steps):
+    """Average duration of the kernel launched by fn(): an event pair around every launch."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in evs])
+    return float(t.mean()), float(np.median(t))
+
+
+class Case:
+    """Device-resident inputs and prepared schedule of one workload."""
+
+    def __init__(self, wl, dense=False, qkv=None):
+        import torch
+        from paper_2606_23019_amd import binding
+        from workloads import masks_for, qkv_for
+        self.wl = wl
+        if dense:
+            n_qb, n_kb = wl.n_qb, wl.n_kb
+            bm = np.ones((wl.H, n_qb, n_kb), dtype=bool)
+            from workloads import pack_rows
+            packed = pack_rows(bm)
+            dens = np.ones(wl.H)
+        else:
+            packed, bm, dens = masks_for(wl)
+        self.packed, self.bm, self.dens = packed, bm, dens
+        self.mask = binding.mask_to_device(packed)
+        self.q, self.k, self.v = qkv if qkv is not None else qkv_for(wl, device="cuda")
+        self.out = torch.empty_like(self.q)
+        self.lse = torch.empty((wl.B, wl.H, wl.N), dtype=torch.float32, device="cuda")
+        self.executed = wl.B * int(bm.sum())
+        self.flops = self.executed * flops_per_block(wl)
+        self.counts, self.lists = binding.mask_prepass(self.mask, wl.H, wl.n_qb, wl.n_kb)
+        self.order = binding.schedule(self.counts, wl.B, wl.H, wl.n_qb)
+        torch.cuda.synchronize()
+
+    def step(self):
+        from paper_2606_23019_amd import binding
+        binding.bsattn_fwd(self.q, self.k, self.v, self.mask, self.wl.blk_q, self.wl.blk_k,
+                           self.wl.scale, out=self.out, lse=self.lse)
+
+    def attention_only(self):
+        from paper_2606_23019_amd import binding
+        binding.bsattn_fwd_prepared(self.q, self.k, self.v, self.counts, self.lists, self.order,
+                                    self.wl.blk_q, self.wl.blk_k, self.wl.scale, out=self.out,
+                                    lse=self.lse)
+
+
+def parity_spot_check(case, n_items=4):
+    """Sampled check of the last output against the CPU reference (not timed)."""
+    import torch
+    import oracle
+    from workloads import sample_items
+    wl = case.wl
+    items = sample_items(wl, case.bm, n_items)
+    worst = dict(out_max_abs=0.0, lse_max_abs=0.0)
+    n_kb = wl.n_kb
+    for (b, h, u) in items:
+        r0, r1 = u * wl.blk_q, min((u + 1) * wl.blk_q, wl.N)
+
+        def bits(t):
+            return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        allowed = oracle.block_mask(case.packed[h:h + 1, u:u + 1], n_kb)[0, 0]
+        ro, rl = oracle.attention_block(bits(case.q[b, h, r0:r1]), bits(case.k[b, h]),
+                                        bits(case.v[b, h]), allowed, wl.blk_k, wl.scale)
+        go = case.out[b, h, r0:r1].float().cpu().numpy()
+        gl = case.lse[b, h, r0:r1].cpu().numpy()
+        worst["out_max_abs"] = max(worst["out_max_abs"], float(np.abs(go - ro).max()))
+        worst["lse_max_abs"] = max(worst["lse_max_abs"], float(np.abs(gl - rl).max()))
+    return worst
+
+
+def cpu_baseline(case, budget_s=12.0, max_items=48):
+    """The CPU reference, as it stands, on a bounded sample of the same workload."""
+    import torch
+    import oracle
+    wl = case.wl
+    rng = np.random.default_rng(wl.sample_seed + 17)
+    n_kb = wl.n_kb
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    # per-head host copies are part of the setup, not of the timed work
+    heads = sorted(set(int(h) for h in rng.integers(0, wl.H, size=4)))
+    host = {}
+    for h in heads:
+        host[h] = tuple(t[0, h].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+                        for t in (case.q, case.k, case.v))
+    items = [(h, int(u)) for h in heads for u in rng.permutation(wl.n_qb)]
+    rng.shuffle(items)
+    done_blocks, n_done, t_used = 0, 0, 0.0
+    for (h, u) in items[:max_items]:
+        qb, kb, vb = host[h]
+        allowed = oracle.block_mask(case.packed[h:h + 1, u:u + 1], n_kb)[0, 0]
+        r0, r1 = u * wl.blk_q, min((u + 1) * wl.blk_q, wl.N)
+        t0 = time.perf_counter()
+        oracle.attention_block(qb[r0:r1], kb, vb, allowed, wl.blk_k, wl.scale)
+        t_used += time.perf_counter() - t0
+        done_blocks += int(allowed.sum())
+        n_done += 1
+        if t_used >= budget_s:
+            break
+    value = done_blocks * flops_per_block(wl) / t_used / 1e12
+    return {"value": value, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d query blocks (%d executed 128x128 blocks) of heads %s of %s, float64 "
+                      "NumPy on %d host threads, %.1f s" % (n_done, done_blocks, heads, wl.name,
+                                                            threads, t_used)}
+
+
+def traffic_record():
+    """HBM bytes per attention launch from the committed counter summary, if it still
+    describes the current kernel source."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_SUMMARY):
+        if ":" in line and not line.startswith("#"):
+            a, b = line.split(":", 1)
+            kv[a.strip()] = b.strip()
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()[:16]
+    if kv.get("kernel_source_sha256_16") != src:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def run_sweep(path, steps, warmup):
+    import torch
+    from workloads import SWEEP_BLKS, SWEEP_KINDS, SWEEP_RHOS, sweep_point
+    rows = []
+    for blk in SWEEP_BLKS:
+        dense_wl = sweep_point(1.0, blk, "structured")
+        dense = Case(dense_wl, dense=True)
+        qkv = (dense.q, dense.k, dense.v)
+        for _ in range(warmup):
+            dense.attention_only()
+        t_dense, _ = _per_launch_time(dense.attention_only, steps)
+        for kind in SWEEP_KINDS:
+            for rho in SWEEP_RHOS:
+                wl = sweep_point(rho, blk, kind)
+                c = dense if rho >= 1.0 else Case(wl, qkv=qkv)
+                for _ in range(warmup):
+                    c.attention_only()
+                t, _ = _per_launch_time(c.attention_only, steps)
+                tf = c.flops / (t * 1e-3) / 1e12
+                rows.append(dict(blk=blk, kind=kind, rho=rho, ms=t, tflops=tf,
+                                 pct_peak=100 * tf / PEAK_BF16_TFLOPS, speedup_vs_dense=t_dense / t,
+                                 speedup_x_rho=rho * t_dense / t))
+                log(json.dumps(rows[-1]))
+                if c is not dense:
+                    del c
+        del dense, qkv
+        torch.cuda.empty_cache()
+    with open(path, "w") as f:
+        json.dump(rows, f, indent=1)
+    return rows
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="14b-480p")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", default=None, help="also run the density/block sweep into this file")
+    ap.add_argument("--configs", default=None, help="also time every named workload into this file")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the block-sparse forward is a single-GPU kernel "
+              "here (heads shard across GPUs with no exchange); run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from workloads import SHORT
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2606_23019_amd import binding
+    binding.load(build_if_missing=True)
+
+    wl = SHORT[args.workload]
+    log("workload", wl.name)
+    case = Case(wl)
+    for _ in range(args.warmup):
+        case.step()
+    torch.cuda.synchronize()
+    ms_step = _events_time(case.step, args.steps)
+    value = case.flops / (ms_step * 1e-3) / 1e12
+
+    # attention kernel alone, event pair around every launch on its stream
+    for _ in range(args.warmup):
+        case.attention_only()
+    ms_attn, ms_attn_med = _per_launch_time(case.attention_only, args.steps)
+    achieved = case.flops / (ms_attn * 1e-3) / 1e12
+
+    # same kernel, all-ones mask, same inputs
+    dense = Case(wl, dense=True, qkv=(case.q, case.k, case.v))
+    dense_steps = max(3, args.steps // 4)
+    for _ in range(2):
+        dense.attention_only()
+    ms_dense, _ = _per_launch_time(dense.attention_only, dense_steps)
+    dense_tflops = dense.flops / (ms_dense * 1e-3) / 1e12
+    del dense
+    torch.cuda.empty_cache()
+
+    case.step()
+    torch.cuda.synchronize()
+    parity = parity_spot_check(case)
+
+    traffic = traffic_record()
+    rec = {
+        "metric": "block-sparse attn fwd effective TFLOP/s",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d,
+            "blk_q": wl.blk_q, "blk_k": wl.blk_k, "mask": wl.mask_kind,
+            "density_range": list(wl.rho_range) if wl.rho_range else wl.rho,
+            "mean_density": round(float(case.dens.mean()), 4),
+            "executed_blocks": case.executed, "executed_tflop": round(case.flops / 1e12, 4),
+        },
+        "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "attention_kernel_ms": round(ms_attn, 4),
+        "attention_kernel_ms_median": round(ms_attn_med, 4),
+        "dense_mask_ms": round(ms_dense, 4),
+        "dense_mask_tflops": round(dense_tflops, 3),
+        "speedup_vs_dense": round(ms_dense / ms_attn, 3),
+        "parity_spot_check": parity,
+        "roofline": {
+            "bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+        },
+    }
+    if args.configs:
+        from workloads import SHORT as ALL
+        res = {}
+        for name, w in ALL.items():
+            c = Case(w)
+            for _ in range(args.warmup):
+                c.attention_only()
+            t, _ = _per_launch_time(c.attention_only, args.steps)
+            res[name] = dict(workload=w.name, ms=t, tflops=c.flops / (t * 1e-3) / 1e12,
+                             mean_density=float(c.dens.mean()), executed_blocks=c.executed)
+            log(json.dumps(res[name]))
+            del c
+            torch.cuda.empty_cache()
+        with open(args.configs, "w") as f:
+            json.dump(res, f, indent=1)
+    if args.sweep:
+        run_sweep(args.sweep, args.steps, args.warmup)
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(case)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,138 @@
+/*
+ * sa_bsattn.h -- block-sparse scaled-dot-product attention forward for
+ * MI355X (gfx950), C ABI.
+ *
+ * The operation is the forward pass of the paper's CRM kernel (Sec. 4.3.2,
+ * "CRM Kernel: Bit-wise Block-Sparse Attention Execution"): attention over
+ * flattened video tokens in which every head follows a static bit-packed
+ * block mask, and only the key blocks whose bit is set are computed.  For
+ * batch b, head h and query token i (query block u = i / blk_q):
+ *
+ *   K_i   = { j < N : bit(h, u, j / blk_k) = 1 }
+ *   s_ij  = scale * <q_i, k_j>
+ *   lse_i = log sum_{j in K_i} exp(s_ij)             (natural log)
+ *   out_i = sum_{j in K_i} exp(s_ij - lse_i) v_j
+ *
+ * A query block with no set bit gets out = 0 and lse = -inf.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor pointers are DEVICE pointers on the current HIP device.  The
+ *   caller owns every buffer; the library never frees or retains them.
+ * - q, k, v, out: bfloat16 (stored as uint16), contiguous [B][H][N][d],
+ *   16-byte aligned.  lse: float32, contiguous [B][H][N], 4-byte aligned.
+ *   out and lse must not overlap any input.
+ * - mask_bits: the Compressed Row Mask of Sec. 4.3.2 stored as little-endian
+ *   uint64 words, contiguous [H][n_qb][W] with n_qb = ceil(N / blk_q),
+ *   n_kb = ceil(N / blk_k), W = ceil(n_kb / 64).  Key block v of row (h, u)
+ *   is bit (v mod 64) of word v / 64 (LSB-first, the enumeration order of the
+ *   paper's CRM forward iterator).  Bits at positions >= n_kb are ignored.
+ *   One mask per head, shared by all batch entries.  8-byte aligned.
+ * - stream: a hipStream_t passed as void* (NULL = the default stream).  All
+ *   work is enqueued on it; no call synchronises unless its comment says so.
+ *   Execution errors surface at the caller's next synchronisation.
+ * - Supported shapes: d in {64, 128}; blk_q == blk_k in {64, 128}; B, H,
+ *   N >= 1; n_kb <= 65535; B * H * n_qb < 2^31.  scale must be finite and > 0.
+ * - Every argument is validated before anything is enqueued: a non-zero
+ *   return means nothing was launched and no output was written.
+ */
+#ifndef SA_BSATTN_H
+#define SA_BSATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SA_API __attribute__((visibility("default")))
+
+/* Status codes. */
+#define SA_OK 0
+#define SA_ERR_INVALID_ARG 1 /* null/misaligned pointer, bad size, bad scale, aliasing */
+#define SA_ERR_UNSUPPORTED 2 /* shape outside the supported set above */
+#define SA_ERR_HIP 3         /* a HIP allocation or launch failed */
+
+/* Human-readable text for a status code (static storage, never NULL). */
+SA_API const char* sa_status_string(int status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+SA_API int sa_version(void);
+
+/*
+ * One-shot forward pass (Sec. 4.3.2): runs the mask pre-pass, the schedule
+ * and the attention kernel on `stream`.  Internal workspace (per-row counts
+ * and key-block lists, the work order) is taken with stream-ordered
+ * hipMallocAsync and released with hipFreeAsync on the same stream.
+ * Returns SA_OK, SA_ERR_INVALID_ARG, SA_ERR_UNSUPPORTED or SA_ERR_HIP.
+ */
+SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v,
+                         const uint64_t* mask_bits, void* out, float* lse,
+                         int B, int H, int N, int d, int blk_q, int blk_k,
+                         float scale, void* stream);
+
+/*
+ * Mask pre-pass alone (the CRM walk of the paper's appendix "CRM Forward
+ * Iterator", done once per row instead of inside the attention loop):
+ * for each row r = h * n_qb + u writes counts[r] = number of set bits
+ * (positions < n_kb) and lists[r * n_kb + 0 .. counts[r]-1] = the enabled key
+ * blocks in ascending order.  Entries past counts[r] are left untouched.
+ * counts: device int32 [H * n_qb]; lists: device uint16 [H * n_qb * n_kb].
+ * Requires 1 <= n_kb <= 65535.
+ */
+SA_API int sa_mask_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb,
+                           int32_t* counts, uint16_t* lists, void* stream);
+
+/*
+ * Work schedule (balances heads of uneven density): writes order[0 .. B*H*n_qb-1],
+ * a permutation of the work items it = (b * H + h) * n_qb + u.  Items of one
+ * (b, h) stay together in ascending u; (b, h) groups are ordered by
+ * decreasing total enabled blocks (largest first, ties by index) so that the
+ * heaviest heads start first.  counts: device int32 [H * n_qb] from the
+ * pre-pass.  order: device int32 [B * H * n_qb].
+ */
+SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb,
+                       int32_t* order, void* stream);
+
+/*
+ * Attention kernel alone, on a pre-computed pre-pass and schedule (the
+ * static-mask case: masks are built once and reused for every prompt,
+ * Sec. 3 overview "Reuse for All Prompts").  counts/lists/order as produced
+ * by sa_mask_prepass and sa_schedule for the same (B, H, N, blk_q, blk_k).
+ */
+SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
+                                  const int32_t* counts, const uint16_t* lists,
+                                  const int32_t* order, void* out, float* lse,
+                                  int B, int H, int N, int d, int blk_q, int blk_k,
+                                  float scale, void* stream);
+
+/*
+ * Plan API for static masks.  sa_bsattn_plan_create allocates the plan's
+ * device buffers with hipMalloc, runs the pre-pass and schedule on `stream`,
+ * then SYNCHRONISES `stream` to record the executed-block count.  The plan
+ * keeps no pointer to mask_bits.  A plan is bound to the device that was
+ * current at creation.  Plans are not thread-safe across concurrent calls on
+ * different streams only in the sense that they are read-only after creation:
+ * concurrent sa_bsattn_fwd_plan calls are allowed.
+ */
+typedef struct sa_plan* sa_plan_t;
+
+SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
+                                 int blk_q, int blk_k, void* stream, sa_plan_t* plan);
+
+/* Attention with a plan: only the attention kernel is enqueued. */
+SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v,
+                              void* out, float* lse, int d, float scale, void* stream);
+
+/* Total executed (b, h, u, v) blocks of the plan: B * sum of all row counts. */
+SA_API int sa_bsattn_plan_stats(sa_plan_t plan, int64_t* executed_blocks);
+
+/* Frees the plan (hipFree, which waits for outstanding work on the device). */
+SA_API int sa_bsattn_plan_destroy(sa_plan_t plan);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SA_BSATTN_H */

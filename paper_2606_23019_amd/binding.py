@@ -1,0 +1,236 @@
+"""ctypes binding of ``libsa_bsattn.so`` (C ABI declared in include/sa_bsattn.h).
+
+Argument marshalling only: every step of the forward pass runs in the HIP
+library.  PyTorch supplies device buffers and the current stream.  There is no
+fallback: if the library cannot be loaded the functions raise.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+SA_OK = 0
+SA_ERR_INVALID_ARG = 1
+SA_ERR_UNSUPPORTED = 2
+SA_ERR_HIP = 3
+
+_LIB = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_F = ctypes.c_float
+
+# name -> (restype, argtypes); mirrors include/sa_bsattn.h
+SIGNATURES = {
+    "sa_status_string": (ctypes.c_char_p, [_I]),
+    "sa_version": (_I, []),
+    "sa_bsattn_fwd": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
+    "sa_mask_prepass": (_I, [_P, _I, _I, _I, _P, _P, _P]),
+    "sa_schedule": (_I, [_P, _I, _I, _I, _P, _P]),
+    "sa_bsattn_fwd_prepared": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
+    "sa_bsattn_plan_create": (_I, [_P, _I, _I, _I, _I, _I, _P, ctypes.POINTER(_P)]),
+    "sa_bsattn_fwd_plan": (_I, [_P, _P, _P, _P, _P, _P, _I, _F, _P]),
+    "sa_bsattn_plan_stats": (_I, [_P, ctypes.POINTER(ctypes.c_int64)]),
+    "sa_bsattn_plan_destroy": (_I, [_P]),
+}
+
+
+class SAError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__("%s failed: %s (status %d)" % (fn, status_string(status), status))
+
+
+def library_path():
+    return _build.LIB_PATH
+
+
+def load(build_if_missing=True):
+    """Load the library (building it in-tree only if it is absent)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        if not build_if_missing:
+            raise RuntimeError("HIP library %s is not built" % path)
+        _build.build()
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def status_string(status):
+    return load().sa_status_string(int(status)).decode()
+
+
+def _check(fn, status):
+    if status != SA_OK:
+        raise SAError(fn, status)
+
+
+# --------------------------------------------------------------- tensors ---
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev_ptr(t, dtype, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch tensor" % name)
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on the GPU, got %s" % (name, t.device))
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def mask_to_device(mask_bits, device="cuda"):
+    """uint64 numpy [H, n_qb, W] -> int64 torch tensor (same bits) on ``device``."""
+    torch = _torch()
+    if isinstance(mask_bits, torch.Tensor):
+        return mask_bits.to(device).contiguous()
+    m = np.ascontiguousarray(mask_bits, dtype=np.uint64).view(np.int64)
+    return torch.from_numpy(m.copy()).to(device)
+
+
+def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None, stream=None):
+    """One-shot forward: ``sa_bsattn_fwd``.  q, k, v: bf16 [B, H, N, d] on the GPU.
+
+    mask_bits: int64/uint64 device tensor (or numpy uint64) [H, n_qb, W].
+    Returns (out bf16 [B, H, N, d], lse float32 [B, H, N]).
+    """
+    torch = _torch()
+    lib = load()
+    B, H, N, d = q.shape
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    m = mask_to_device(mask_bits, q.device)
+    if m.dtype == torch.uint64:
+        m = m.view(torch.int64)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    st = lib.sa_bsattn_fwd(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+        _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(m, torch.int64, "mask_bits"),
+        _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
+        B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
+    _check("sa_bsattn_fwd", st)
+    return out, lse
+
+
+def mask_prepass(mask_bits, H, n_qb, n_kb, stream=None):
+    """``sa_mask_prepass``: returns (counts int32 [H*n_qb], lists int16-as-uint16 [H*n_qb, n_kb])."""
+    torch = _torch()
+    lib = load()
+    m = mask_to_device(mask_bits)
+    counts = torch.full((H * n_qb,), -1, dtype=torch.int32, device=m.device)
+    lists = torch.full((H * n_qb, n_kb), -1, dtype=torch.int16, device=m.device)
+    st = lib.sa_mask_prepass(_dev_ptr(m, torch.int64, "mask_bits"), H, n_qb, n_kb,
+                             _dev_ptr(counts, torch.int32, "counts"),
+                             _dev_ptr(lists, torch.int16, "lists"), _stream(stream))
+    _check("sa_mask_prepass", st)
+    return counts, lists
+
+
+def schedule(counts, B, H, n_qb, stream=None):
+    """``sa_schedule``: returns order int32 [B*H*n_qb]."""
+    torch = _torch()
+    lib = load()
+    order = torch.full((B * H * n_qb,), -1, dtype=torch.int32, device=counts.device)
+    st = lib.sa_schedule(_dev_ptr(counts, torch.int32, "counts"), B, H, n_qb,
+                         _dev_ptr(order, torch.int32, "order"), _stream(stream))
+    _check("sa_schedule", st)
+    return order
+
+
+def bsattn_fwd_prepared(q, k, v, counts, lists, order, blk_q, blk_k, scale=None, out=None,
+                        lse=None, stream=None):
+    """``sa_bsattn_fwd_prepared``: attention kernel on a given pre-pass and schedule."""
+    torch = _torch()
+    lib = load()
+    B, H, N, d = q.shape
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    st = lib.sa_bsattn_fwd_prepared(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+        _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(counts, torch.int32, "counts"),
+        _dev_ptr(lists, torch.int16, "lists"), _dev_ptr(order, torch.int32, "order"),
+        _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
+        B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
+    _check("sa_bsattn_fwd_prepared", st)
+    return out, lse
+
+
+class Plan:
+    """Static-mask plan (``sa_bsattn_plan_*``): pre-pass and schedule done once."""
+
+    def __init__(self, mask_bits, B, H, N, blk_q, blk_k, stream=None):
+        torch = _torch()
+        self._lib = load()
+        self._m = mask_to_device(mask_bits)
+        self.B, self.H, self.N, self.blk_q, self.blk_k = B, H, N, blk_q, blk_k
+        h = ctypes.c_void_p()
+        st = self._lib.sa_bsattn_plan_create(_dev_ptr(self._m, torch.int64, "mask_bits"), B, H, N,
+                                             blk_q, blk_k, _stream(stream), ctypes.byref(h))
+        _check("sa_bsattn_plan_create", st)
+        self._h = h
+
+    @property
+    def executed_blocks(self):
+        n = ctypes.c_int64()
+        _check("sa_bsattn_plan_stats", self._lib.sa_bsattn_plan_stats(self._h, ctypes.byref(n)))
+        return n.value
+
+    def __call__(self, q, k, v, scale=None, out=None, lse=None, stream=None):
+        torch = _torch()
+        B, H, N, d = q.shape
+        if (B, H, N) != (self.B, self.H, self.N):
+            raise ValueError("q shape %s does not match the plan" % (tuple(q.shape),))
+        if scale is None:
+            scale = 1.0 / float(d) ** 0.5
+        if out is None:
+            out = torch.empty_like(q)
+        if lse is None:
+            lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+        st = self._lib.sa_bsattn_fwd_plan(
+            self._h, _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+            _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, torch.bfloat16, "out"),
+            _dev_ptr(lse, torch.float32, "lse"), d, float(scale), _stream(stream))
+        _check("sa_bsattn_fwd_plan", st)
+        return out, lse
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.sa_bsattn_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

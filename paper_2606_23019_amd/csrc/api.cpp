@@ -1,0 +1,235 @@
+// C ABI of the block-sparse attention library (declared in include/sa_bsattn.h).
+//
+// Every entry point validates all arguments before enqueuing anything, so a
+// non-zero status means no kernel ran and no output was written.
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <new>
+
+#include "../../include/sa_bsattn.h"
+#include "launch.h"
+
+namespace {
+
+constexpr int kVersion = 100;  // 0.1.0
+
+struct Dims {
+  int n_qb, n_kb, W;
+};
+
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+inline bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return na && nb && x < y + nb && y < x + na;
+}
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Shape checks shared by every entry point that takes (B, H, N, blk_q, blk_k).
+int check_shape(int B, int H, int N, int blk_q, int blk_k, Dims* dims) {
+  if (B < 1 || H < 1 || N < 1) return SA_ERR_INVALID_ARG;
+  if (blk_q != blk_k || (blk_q != 64 && blk_q != 128)) return SA_ERR_UNSUPPORTED;
+  const int n_qb = (N + blk_q - 1) / blk_q;
+  const int n_kb = (N + blk_k - 1) / blk_k;
+  if (n_kb > 65535) return SA_ERR_UNSUPPORTED;
+  if ((int64_t)B * H * n_qb >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
+  dims->n_qb = n_qb;
+  dims->n_kb = n_kb;
+  dims->W = (n_kb + 63) / 64;
+  return SA_OK;
+}
+
+int check_tensors(const void* q, const void* k, const void* v, const void* mask_bits, int mask_words,
+                  const void* out, const float* lse, int B, int H, int N, int d, float scale) {
+  if (d != 64 && d != 128) return SA_ERR_UNSUPPORTED;
+  if (!(scale > 0.f) || !isfinite(scale)) return SA_ERR_INVALID_ARG;
+  if (!q || !k || !v || !out || !lse) return SA_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(lse, 4))
+    return SA_ERR_INVALID_ARG;
+  const size_t tensor_bytes = (size_t)B * H * N * d * 2;
+  const size_t lse_bytes = (size_t)B * H * N * 4;
+  const size_t mask_bytes = (size_t)mask_words * 8;
+  const void* ins[4] = {q, k, v, mask_bits};
+  const size_t in_bytes[4] = {tensor_bytes, tensor_bytes, tensor_bytes, mask_bytes};
+  for (int i = 0; i < 4; ++i) {
+    if (!ins[i]) continue;
+    if (overlap(out, tensor_bytes, ins[i], in_bytes[i])) return SA_ERR_INVALID_ARG;
+    if (overlap(lse, lse_bytes, ins[i], in_bytes[i])) return SA_ERR_INVALID_ARG;
+  }
+  if (overlap(out, tensor_bytes, lse, lse_bytes)) return SA_ERR_INVALID_ARG;
+  return SA_OK;
+}
+
+struct Workspace {
+  size_t counts_off, lists_off, order_off, total;
+};
+
+Workspace plan_workspace(int B, int H, const Dims& dm) {
+  Workspace w;
+  const size_t rows = (size_t)H * dm.n_qb;
+  w.counts_off = 0;
+  w.lists_off = align_up(rows * 4, 256);
+  w.order_off = w.lists_off + align_up(rows * dm.n_kb * 2, 256);
+  w.total = w.order_off + align_up((size_t)B * H * dm.n_qb * 4, 256);
+  return w;
+}
+
+}  // namespace
+
+struct sa_plan {
+  int B, H, N, blk_q, blk_k;
+  Dims dims;
+  int device;
+  void* buf;
+  int32_t* counts;
+  uint16_t* lists;
+  int32_t* order;
+  int64_t executed;
+};
+
+extern "C" {
+
+SA_API const char* sa_status_string(int status) {
+  switch (status) {
+    case SA_OK: return "ok";
+    case SA_ERR_INVALID_ARG: return "invalid argument";
+    case SA_ERR_UNSUPPORTED: return "unsupported shape";
+    case SA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+SA_API int sa_version(void) { return kVersion; }
+
+SA_API int sa_mask_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,
+                           uint16_t* lists, void* stream) {
+  if (!mask_bits || !counts || !lists || H < 1 || n_qb < 1 || n_kb < 1) return SA_ERR_INVALID_ARG;
+  if (!aligned(mask_bits, 8) || !aligned(counts, 4) || !aligned(lists, 2)) return SA_ERR_INVALID_ARG;
+  if (n_kb > 65535 || (int64_t)H * n_qb >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
+  const hipError_t e =
+      sa::launch_prepass(mask_bits, H, n_qb, n_kb, counts, lists, (hipStream_t)stream);
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* order, void* stream) {
+  if (!counts || !order || B < 1 || H < 1 || n_qb < 1) return SA_ERR_INVALID_ARG;
+  if (!aligned(counts, 4) || !aligned(order, 4)) return SA_ERR_INVALID_ARG;
+  if ((int64_t)B * H * n_qb >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
+  const hipError_t e = sa::launch_schedule(counts, B, H, n_qb, order, (hipStream_t)stream);
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
+                                  const int32_t* counts, const uint16_t* lists,
+                                  const int32_t* order, void* out, float* lse, int B, int H, int N,
+                                  int d, int blk_q, int blk_k, float scale, void* stream) {
+  Dims dm;
+  int st = check_shape(B, H, N, blk_q, blk_k, &dm);
+  if (st != SA_OK) return st;
+  st = check_tensors(q, k, v, nullptr, 0, out, lse, B, H, N, d, scale);
+  if (st != SA_OK) return st;
+  if (!counts || !lists || !order) return SA_ERR_INVALID_ARG;
+  sa::AttnArgs a{q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k,
+                 dm.n_qb, dm.n_kb, scale};
+  return sa::launch_attention(a, (hipStream_t)stream) == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
+                         void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
+                         float scale, void* stream) {
+  Dims dm;
+  int st = check_shape(B, H, N, blk_q, blk_k, &dm);
+  if (st != SA_OK) return st;
+  if (!mask_bits || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
+  st = check_tensors(q, k, v, mask_bits, H * dm.n_qb * dm.W, out, lse, B, H, N, d, scale);
+  if (st != SA_OK) return st;
+
+  hipStream_t s = (hipStream_t)stream;
+  const Workspace w = plan_workspace(B, H, dm);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, w.total, s) != hipSuccess || !ws) return SA_ERR_HIP;
+  char* base = (char*)ws;
+  int32_t* counts = (int32_t*)(base + w.counts_off);
+  uint16_t* lists = (uint16_t*)(base + w.lists_off);
+  int32_t* order = (int32_t*)(base + w.order_off);
+  hipError_t e = sa::launch_prepass(mask_bits, H, dm.n_qb, dm.n_kb, counts, lists, s);
+  if (e == hipSuccess) e = sa::launch_schedule(counts, B, H, dm.n_qb, order, s);
+  if (e == hipSuccess) {
+    sa::AttnArgs a{q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k,
+                   dm.n_qb, dm.n_kb, scale};
+    e = sa::launch_attention(a, s);
+  }
+  const hipError_t ef = hipFreeAsync(ws, s);
+  return (e == hipSuccess && ef == hipSuccess) ? SA_OK : SA_ERR_HIP;
+}
+
+SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N, int blk_q,
+                                 int blk_k, void* stream, sa_plan_t* plan) {
+  if (!plan) return SA_ERR_INVALID_ARG;
+  *plan = nullptr;
+  Dims dm;
+  int st = check_shape(B, H, N, blk_q, blk_k, &dm);
+  if (st != SA_OK) return st;
+  if (!mask_bits || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  sa_plan* p = new (std::nothrow) sa_plan();
+  if (!p) return SA_ERR_HIP;
+  p->B = B; p->H = H; p->N = N; p->blk_q = blk_q; p->blk_k = blk_k; p->dims = dm;
+  if (hipGetDevice(&p->device) != hipSuccess) { delete p; return SA_ERR_HIP; }
+  const Workspace w = plan_workspace(B, H, dm);
+  if (hipMalloc(&p->buf, w.total) != hipSuccess) { delete p; return SA_ERR_HIP; }
+  char* base = (char*)p->buf;
+  p->counts = (int32_t*)(base + w.counts_off);
+  p->lists = (uint16_t*)(base + w.lists_off);
+  p->order = (int32_t*)(base + w.order_off);
+  hipError_t e = sa::launch_prepass(mask_bits, H, dm.n_qb, dm.n_kb, p->counts, p->lists, s);
+  if (e == hipSuccess) e = sa::launch_schedule(p->counts, B, H, dm.n_qb, p->order, s);
+  int32_t* host_counts = nullptr;
+  const size_t rows = (size_t)H * dm.n_qb;
+  if (e == hipSuccess) {
+    host_counts = new (std::nothrow) int32_t[rows];
+    if (!host_counts) e = hipErrorOutOfMemory;
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(host_counts, p->counts, rows * 4, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    delete[] host_counts;
+    (void)hipFree(p->buf);
+    delete p;
+    return SA_ERR_HIP;
+  }
+  int64_t tot = 0;
+  for (size_t i = 0; i < rows; ++i) tot += host_counts[i];
+  delete[] host_counts;
+  p->executed = tot * B;
+  *plan = p;
+  return SA_OK;
+}
+
+SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v,
+                              void* out, float* lse, int d, float scale, void* stream) {
+  if (!plan) return SA_ERR_INVALID_ARG;
+  return sa_bsattn_fwd_prepared(q, k, v, plan->counts, plan->lists, plan->order, out, lse, plan->B,
+                                plan->H, plan->N, d, plan->blk_q, plan->blk_k, scale, stream);
+}
+
+SA_API int sa_bsattn_plan_stats(sa_plan_t plan, int64_t* executed_blocks) {
+  if (!plan || !executed_blocks) return SA_ERR_INVALID_ARG;
+  *executed_blocks = plan->executed;
+  return SA_OK;
+}
+
+SA_API int sa_bsattn_plan_destroy(sa_plan_t plan) {
+  if (!plan) return SA_ERR_INVALID_ARG;
+  const hipError_t e = hipFree(plan->buf);
+  delete plan;
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,250 @@
+// Block-sparse attention forward for gfx950 (CDNA4).
+//
+// What it computes (paper Sec. 4.3.2): FlashAttention's forward pass with the
+// dense key-block loop replaced by a walk over the key blocks enabled in the
+// query block's Compressed Row Mask row.  Each executed block is a dense
+// 128 x 128 (or 64 x 64) tile, so both contractions run on the matrix cores.
+//
+// Work item = (b, h, query block u); one workgroup per item, BQ / 32
+// wavefronts, each owning 32 query rows.  Per enabled key block kb:
+//
+//   1. the workgroup copies K[kb] and V[kb] (BK x D bf16, row-major) from
+//      global memory into LDS (16-byte chunks, XOR-swizzled per row);
+//   2. every wavefront computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16:
+//      Q^T (its 32 queries) stays in registers as the B operand, K rows come
+//      from LDS as the A operand.  In the transposed product each lane owns
+//      one query column, so the row statistics of the softmax are lane-local
+//      apart from one exchange between the two half-wavefronts;
+//   3. online softmax in fp32 in the log2 domain: running max m and sum l,
+//      p = exp2(s * scale * log2(e) - m), the accumulator rescaled by
+//      exp2(m_old - m_new);
+//   4. O^T += V^T P^T, again 32x32x16 MFMA: P (rounded to bf16) is already
+//      in the B-operand layout -- the K rows were fed to the first product
+//      in an order that makes this so -- and V^T comes from LDS through the
+//      gfx950 transposing read ds_read_b64_tr_b16.
+//
+// Epilogue: out = O / l rounded to bf16, lse = (m + log2 l) ln 2.
+// Keys past N (ragged last block) are loaded as zeros and get -inf logits.
+
+#include <math.h>
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace sa {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <int BQ, int BK, int D>
+struct Tile {
+  static constexpr int kWaves = BQ / 32;
+  static constexpr int kThreads = kWaves * 64;
+  static constexpr int kChunksPerRow = D / 8;  // 16-byte chunks
+  static constexpr int kChunksPerThread = BK * kChunksPerRow / kThreads;
+  static_assert(BQ % 32 == 0 && BK % 32 == 0 && D % 32 == 0, "tile shape");
+  static_assert((BK * kChunksPerRow) % kThreads == 0, "staging split");
+};
+
+// XOR applied to the 16-byte chunk index of LDS row r.
+//  K tile: MFMA A-operand reads touch rows {0..3, 8..11} (and {4..7, 12..15})
+//  together; these XORs are distinct over each such set.
+//  V tile: a transposing read touches 4 consecutive rows x 2 chunks per
+//  16 lanes; XOR by 0, 2, 4, 6 spreads them over distinct banks.
+__device__ __forceinline__ int swz_k(int r) { return (r & 3) | ((r >> 1) & 4); }
+__device__ __forceinline__ int swz_v(int r) { return (r & 3) << 1; }
+
+// Key (within a 32-key group) fed to MFMA row m: bits 2 and 3 of m swapped.
+// With this order, register i of the S^T accumulator of lane l holds key
+// 16 * (i / 8) + 8 * (l / 32) + (i % 8): eight consecutive keys per half
+// wavefront, exactly the B-operand layout of the following P V product.
+__device__ __forceinline__ int key_of_row(int m) {
+  return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+// Copy rows key0 .. key0 + BK - 1 of a [N][D] bf16 matrix into an LDS tile,
+// 16-byte chunks XOR-swizzled per row; rows >= N are filled with zeros.
+template <typename T, int D, typename Swz>
+__device__ __forceinline__ void stage_tile(__bf16* lds, const __bf16* src, int key0, int N, int tid,
+                                           Swz swz) {
+  u32x4 r4[T::kChunksPerThread];
+#pragma unroll
+  for (int i = 0; i < T::kChunksPerThread; ++i) {
+    const int cidx = i * T::kThreads + tid;
+    const int r = cidx / T::kChunksPerRow;
+    const int cc = cidx % T::kChunksPerRow;
+    const int key = key0 + r;
+    r4[i] = key < N ? *(const u32x4*)(src + (int64_t)key * D + cc * 8) : u32x4{};
+  }
+#pragma unroll
+  for (int i = 0; i < T::kChunksPerThread; ++i) {
+    const int cidx = i * T::kThreads + tid;
+    const int r = cidx / T::kChunksPerRow;
+    const int cc = cidx % T::kChunksPerRow;
+    lds_write_b128(lds + r * D + ((cc ^ swz(r)) << 3), r4[i]);
+  }
+}
+
+template <int BQ, int BK, int D>
+__global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const int32_t* __restrict__ counts, const uint16_t* __restrict__ lists,
+    const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
+    int N, int n_qb, int n_kb, float c_log2) {
+  using T = Tile<BQ, BK, D>;
+  __shared__ __attribute__((aligned(16))) __bf16 Ks[BK * D];
+  __shared__ __attribute__((aligned(16))) __bf16 Vs[BK * D];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int half = lane >> 5;
+  const int l32 = lane & 31;
+
+  const int item = order[blockIdx.x];
+  const int bh = item / n_qb;
+  const int u = item - bh * n_qb;
+  const int h = bh % H;
+  const int row = h * n_qb + u;
+  const int cnt = counts[row];
+  const uint16_t* list = lists + (int64_t)row * n_kb;
+  const int64_t base = (int64_t)bh * N * D;
+  const __bf16* Qb = Q + base;
+  const __bf16* Kb = K + base;
+  const __bf16* Vb = V + base;
+
+  // Q^T fragments (B operand): lane holds Q[qrow][16 dc + 8 half .. +7].
+  const int qrow = u * BQ + wave * 32 + l32;
+  bf16x8 qf[D / 16];
+#pragma unroll
+  for (int dc = 0; dc < D / 16; ++dc) {
+    if (qrow < N)
+      qf[dc] = *(const bf16x8*)(Qb + (int64_t)qrow * D + dc * 16 + half * 8);
+    else
+      qf[dc] = bf16x8{};
+  }
+
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int dg = 0; dg < D / 32; ++dg) o[dg] = f32x16{};
+  float m_run = -INFINITY;  // running max of the log2-domain logits
+  float l_run = 0.f;        // this lane's share of the running sum
+
+  for (int t = 0; t < cnt; ++t) {
+    const int key0 = (int)list[t] * BK;
+    __syncthreads();  // previous block's LDS reads are done
+    stage_tile<T, D>(Ks, Kb, key0, N, tid, [](int r) { return swz_k(r); });
+    stage_tile<T, D>(Vs, Vb, key0, N, tid, [](int r) { return swz_v(r); });
+    __syncthreads();
+
+    // S^T = K Q^T, one 32-key group per accumulator.
+    f32x16 s[BK / 32];
+#pragma unroll
+    for (int kg = 0; kg < BK / 32; ++kg) {
+      s[kg] = f32x16{};
+      const int kr = kg * 32 + key_of_row(l32);
+#pragma unroll
+      for (int dc = 0; dc < D / 16; ++dc) {
+        const bf16x8 a = lds_read_b128(Ks + kr * D + (((2 * dc + half) ^ swz_k(kr)) << 3));
+        s[kg] = mfma32x32x16(a, qf[dc], s[kg]);
+      }
+    }
+
+    if (key0 + BK > N) {  // ragged last block: keys >= N do not exist
+#pragma unroll
+      for (int kg = 0; kg < BK / 32; ++kg)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = key0 + kg * 32 + 16 * (i >> 3) + 8 * half + (i & 7);
+          if (key >= N) s[kg][i] = -INFINITY;
+        }
+    }
+
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kg = 0; kg < BK / 32; ++kg)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kg][i]);
+    mx = fmaxf(mx, other_half(mx));
+    const float m_new = fmaxf(m_run, mx * c_log2);
+    const float alpha = fast_exp2(m_run - m_new);
+
+    bf16x8 pf[BK / 16];
+    float lsum = 0.f;
+#pragma unroll
+    for (int kg = 0; kg < BK / 32; ++kg)
+#pragma unroll
+      for (int j8 = 0; j8 < 2; ++j8)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = fast_exp2(fmaf(s[kg][8 * j8 + e], c_log2, -m_new));
+          lsum += p;
+          pf[2 * kg + j8][e] = (__bf16)p;
+        }
+    l_run = l_run * alpha + lsum;
+    m_run = m_new;
+#pragma unroll
+    for (int dg = 0; dg < D / 32; ++dg) o[dg] *= alpha;
+
+    // O^T += V^T P^T.  Lane group g = lane / 16 covers d0 = 32 dg + 16 (g & 1)
+    // and keys 16 c + 8 (g >> 1) + 0..7 (two transposing reads of 4 rows).
+    const int g = lane >> 4;
+    const int j = lane & 15;
+#pragma unroll
+    for (int dg = 0; dg < D / 32; ++dg) {
+      const int dd = dg * 32 + 16 * (g & 1) + (j & 3) * 4;
+#pragma unroll
+      for (int c = 0; c < BK / 16; ++c) {
+        const int r0 = c * 16 + 8 * (g >> 1) + (j >> 2);
+        const int off = (((dd >> 3) ^ swz_v(r0)) << 3) + (dd & 7);  // same XOR for r0 + 4
+        const bf16x4 lo = lds_read_tr16_b64(Vs + r0 * D + off);
+        const bf16x4 hi = lds_read_tr16_b64(Vs + (r0 + 4) * D + off);
+        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        o[dg] = mfma32x32x16(a, pf[c], o[dg]);
+      }
+    }
+  }
+
+  const float l_tot = l_run + other_half(l_run);
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  if (qrow < N) {
+    if (half == 0)
+      LSE[(int64_t)bh * N + qrow] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
+    __bf16* orow = O + base + (int64_t)qrow * D;
+#pragma unroll
+    for (int dg = 0; dg < D / 32; ++dg)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const bf16x4 w = {(__bf16)(o[dg][4 * r4 + 0] * inv), (__bf16)(o[dg][4 * r4 + 1] * inv),
+                          (__bf16)(o[dg][4 * r4 + 2] * inv), (__bf16)(o[dg][4 * r4 + 3] * inv)};
+        *(bf16x4*)(orow + dg * 32 + 8 * r4 + 4 * half) = w;
+      }
+  }
+}
+
+template <int BQ, int BK, int D>
+hipError_t launch_tile(const AttnArgs& a, hipStream_t stream) {
+  const int64_t n_items = (int64_t)a.B * a.H * a.n_qb;
+  hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D>), dim3((unsigned)n_items),
+                     dim3(Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
+                     (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
+                     (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
+  if (a.blk_q == 128 && a.blk_k == 128) {
+    if (a.d == 128) return launch_tile<128, 128, 128>(a, stream);
+    if (a.d == 64) return launch_tile<128, 128, 64>(a, stream);
+  } else if (a.blk_q == 64 && a.blk_k == 64) {
+    if (a.d == 128) return launch_tile<64, 64, 128>(a, stream);
+    if (a.d == 64) return launch_tile<64, 64, 64>(a, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace sa

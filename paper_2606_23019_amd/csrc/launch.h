@@ -1,0 +1,34 @@
+// Internal host-side launchers shared by the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sa {
+
+// Largest B * H for which the schedule sorts (b, h) groups by cost; larger
+// problems keep the natural item order.
+constexpr int kScheduleMaxUnits = 4096;
+
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* counts;
+  const uint16_t* lists;
+  const int32_t* order;
+  void* out;
+  float* lse;
+  int B, H, N, d, blk_q, blk_k, n_qb, n_kb;
+  float scale;
+};
+
+hipError_t launch_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,
+                          uint16_t* lists, hipStream_t stream);
+
+hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* order,
+                           hipStream_t stream);
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
+
+}  // namespace sa

@@ -1,0 +1,135 @@
+// Mask pre-pass and work schedule.
+//
+// Pre-pass: the paper walks each Compressed Row Mask inside the attention
+// kernel with a bit-scan iterator (Sec. 4.3.2 and the appendix "CRM Forward
+// Iterator": skip empty segments, report base + count-trailing-zeros, clear
+// the lowest bit).  Masks are static, so here the walk runs once per row in
+// a separate kernel: one wavefront per row, lane w owns word w, a popcount
+// plus a wavefront prefix sum gives every lane its output offset, and the
+// ctz / clear-lowest loop writes the enabled key blocks in ascending order.
+// The attention kernel then reads a dense list instead of decoding bits.
+//
+// Schedule: heads have very different densities, so (b, h) groups are
+// started heaviest first.  One workgroup computes each head's total enabled
+// blocks, sorts the groups with a bitonic network in LDS, and writes the item
+// order; items inside a group stay in ascending query-block order so that
+// neighbouring query blocks, which share most key blocks in structured
+// masks, run close together in time.
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace sa {
+
+namespace {
+
+constexpr int kPrepassWaves = 4;
+
+__global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
+    const uint64_t* __restrict__ mask, int rows, int n_kb, int W, int32_t* __restrict__ counts,
+    uint16_t* __restrict__ lists) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * kPrepassWaves + (threadIdx.x >> 6);
+  if (row >= rows) return;  // uniform per wavefront
+  const uint64_t* mrow = mask + (int64_t)row * W;
+  uint16_t* lrow = lists + (int64_t)row * n_kb;
+  int done = 0;  // blocks already written for this row
+  for (int w0 = 0; w0 < W; w0 += 64) {
+    const int w = w0 + lane;
+    uint64_t word = 0;
+    if (w < W) {
+      word = mrow[w];
+      const int real = n_kb - w * 64;  // bits of this word that name a real key block
+      if (real < 64) word &= (1ull << real) - 1ull;  // real >= 1 for w < W
+    }
+    const int pc = __popcll(word);
+    int incl = pc;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    int pos = done + incl - pc;
+    while (word) {
+      const int b = __builtin_ctzll(word);
+      lrow[pos++] = (uint16_t)(w * 64 + b);
+      word &= word - 1ull;
+    }
+    done += __shfl(incl, 63, 64);
+  }
+  if (lane == 0) counts[row] = done;
+}
+
+constexpr int kSchedThreads = 1024;
+
+__global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ counts,
+                                                                  int B, int H, int n_qb,
+                                                                  int32_t* __restrict__ order) {
+  __shared__ uint64_t keys[kScheduleMaxUnits];
+  __shared__ uint32_t head_cost[kScheduleMaxUnits];
+  const int tid = threadIdx.x;
+  const int n_units = B * H;
+  const int64_t n_items = (int64_t)n_units * n_qb;
+  if (n_units > kScheduleMaxUnits) {
+    for (int64_t i = tid; i < n_items; i += kSchedThreads) order[i] = (int32_t)i;
+    return;
+  }
+  for (int h = tid; h < H; h += kSchedThreads) {
+    uint32_t c = 0;
+    for (int u = 0; u < n_qb; ++u) c += (uint32_t)counts[(int64_t)h * n_qb + u];
+    head_cost[h] = c;
+  }
+  int P = 1;
+  while (P < n_units) P <<= 1;
+  __syncthreads();
+  // Ascending sort of (~cost, index): decreasing cost, ties by increasing index.
+  for (int i = tid; i < P; i += kSchedThreads) {
+    keys[i] = (i < n_units)
+                  ? ((uint64_t)(0xFFFFFFFFu - head_cost[i % H]) << 32) | (uint32_t)i
+                  : ~0ull;
+  }
+  __syncthreads();
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < P; i += kSchedThreads) {
+        const int p = i ^ j;
+        if (p > i) {
+          const uint64_t a = keys[i], b = keys[p];
+          const bool up = (i & k) == 0;
+          if ((a > b) == up) {
+            keys[i] = b;
+            keys[p] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int64_t i = tid; i < n_items; i += kSchedThreads) {
+    const int p = (int)(i / n_qb);
+    const int u = (int)(i - (int64_t)p * n_qb);
+    const int unit = (int)(keys[p] & 0xFFFFFFFFu);
+    order[i] = unit * n_qb + u;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,
+                          uint16_t* lists, hipStream_t stream) {
+  const int rows = H * n_qb;
+  const int W = (n_kb + 63) / 64;
+  const int grid = (rows + kPrepassWaves - 1) / kPrepassWaves;
+  hipLaunchKernelGGL(prepass_kernel, dim3(grid), dim3(64 * kPrepassWaves), 0, stream, mask_bits,
+                     rows, n_kb, W, counts, lists);
+  return hipGetLastError();
+}
+
+hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* order,
+                           hipStream_t stream) {
+  hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), 0, stream, counts, B, H, n_qb,
+                     order);
+  return hipGetLastError();
+}
+
+}  // namespace sa

@@ -1,0 +1,74 @@
+"""Shared helpers for the GPU parity tests: tolerances and reference runs."""
+
+import numpy as np
+
+import oracle
+
+# Tolerances fixed for the forward pass: out max-abs 2e-2, mean-abs 2e-3; lse max-abs 1e-3.
+OUT_MAX_ABS = 2e-2
+OUT_MEAN_ABS = 2e-3
+LSE_MAX_ABS = 1e-3
+# Where a bf16 output cannot come within OUT_MAX_ABS of the exact value (its
+# half-ulp exceeds 1e-2 once |out| >= 8), the bound is the half-ulp plus the
+# arithmetic allowance below.
+BF16_FLOOR_EXTRA = 4e-3
+
+
+def bf16_half_ulp(x):
+    """Half a unit in the last place of bf16 (8 significant bits) at |x|."""
+    ax = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), 2.0 ** -126)
+    return 2.0 ** (np.floor(np.log2(ax)) - 8)
+
+
+def compare(out_gpu, lse_gpu, out_ref, lse_ref):
+    """Element-wise comparison; returns a stats dict (raises AssertionError on failure)."""
+    out_gpu = np.asarray(out_gpu, dtype=np.float64)
+    out_ref = np.asarray(out_ref, dtype=np.float64)
+    lse_gpu = np.asarray(lse_gpu, dtype=np.float64)
+    lse_ref = np.asarray(lse_ref, dtype=np.float64)
+    assert out_gpu.shape == out_ref.shape and lse_gpu.shape == lse_ref.shape
+    err = np.abs(out_gpu - out_ref)
+    allowed = np.maximum(OUT_MAX_ABS, bf16_half_ulp(out_ref) + BF16_FLOOR_EXTRA)
+    fin_ref = np.isfinite(lse_ref)
+    assert np.array_equal(np.isfinite(lse_gpu), fin_ref), "lse finiteness differs"
+    assert np.all(np.isneginf(lse_gpu[~fin_ref])), "empty rows must have lse = -inf"
+    lse_err = np.abs(lse_gpu[fin_ref] - lse_ref[fin_ref])
+    stats = dict(
+        out_max_abs=float(err.max()) if err.size else 0.0,
+        out_mean_abs=float(err.mean()) if err.size else 0.0,
+        lse_max_abs=float(lse_err.max()) if lse_err.size else 0.0,
+        n_bf16_floor=int((allowed > OUT_MAX_ABS).sum()),
+        out_max_abs_excl_floor=float(err[allowed <= OUT_MAX_ABS].max()) if err.size else 0.0,
+    )
+    assert np.all(np.isfinite(out_gpu)), "non-finite output"
+    bad = err > allowed
+    assert not bad.any(), "out error %.3g at %s exceeds bound (stats %s)" % (
+        err[bad].max(), np.argwhere(bad)[0].tolist(), stats)
+    assert stats["out_mean_abs"] <= OUT_MEAN_ABS, stats
+    assert stats["lse_max_abs"] <= LSE_MAX_ABS, stats
+    return stats
+
+
+def to_bits(t):
+    """bf16 torch tensor -> host uint16 bit array."""
+    import torch
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def reference_items(q, k, v, packed, blk_q, blk_k, scale, items):
+    """Reference (out, lse) for (b, h, u) query blocks, reading device tensors per head."""
+    B, H, N, d = q.shape
+    n_kb = -(-N // blk_k)
+    res = {}
+    by_head = {}
+    for it in items:
+        by_head.setdefault((it[0], it[1]), []).append(it[2])
+    for (b, h), us in sorted(by_head.items()):
+        kb = to_bits(k[b, h])
+        vb = to_bits(v[b, h])
+        allowed = oracle.block_mask(packed[h:h + 1], n_kb)[0]
+        for u in us:
+            r0, r1 = u * blk_q, min((u + 1) * blk_q, N)
+            qb = to_bits(q[b, h, r0:r1])
+            res[(b, h, u)] = oracle.attention_block(qb, kb, vb, allowed[u], blk_k, scale)
+    return res

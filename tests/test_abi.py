@@ -1,0 +1,93 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching the GPU (no compute calls here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_23019_amd import binding
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "sa_bsattn.h")
+
+
+def declared_symbols():
+    txt = open(HEADER).read()
+    return re.findall(r"SA_API\s+[\w\s\*]+?\b(sa_\w+)\s*\(", txt)
+
+
+def test_header_declares_the_boundary():
+    names = declared_symbols()
+    for n in ("sa_bsattn_fwd", "sa_mask_prepass", "sa_schedule", "sa_bsattn_plan_create",
+              "sa_bsattn_fwd_plan", "sa_bsattn_plan_destroy", "sa_status_string"):
+        assert n in names
+    assert set(names) == set(binding.SIGNATURES)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert binding.status_string(0) == "ok"
+    assert "invalid" in binding.status_string(1)
+    assert "unsupported" in binding.status_string(2)
+    assert binding.status_string(99) == "unknown status"
+    assert lib.sa_version() >= 100
+
+
+# Fake device addresses: validation rejects these calls before any HIP call.
+A = 1 << 40
+MB = 1 << 30
+
+
+def _fwd(lib, q=A, k=A + MB, v=A + 2 * MB, m=A + 3 * MB, out=A + 4 * MB, lse=A + 5 * MB,
+         B=1, H=2, N=256, d=128, bq=128, bk=128, scale=0.088):
+    P = ctypes.c_void_p
+    return lib.sa_bsattn_fwd(P(q), P(k), P(v), P(m), P(out), P(lse), B, H, N, d, bq, bk,
+                             ctypes.c_float(scale), None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=0), binding.SA_ERR_INVALID_ARG),
+    (dict(m=0), binding.SA_ERR_INVALID_ARG),
+    (dict(lse=0), binding.SA_ERR_INVALID_ARG),
+    (dict(q=A + 8), binding.SA_ERR_INVALID_ARG),             # misaligned
+    (dict(m=A + 3 * MB + 4), binding.SA_ERR_INVALID_ARG),    # misaligned mask
+    (dict(out=A + 16), binding.SA_ERR_INVALID_ARG),          # out overlaps q
+    (dict(lse=A + 2 * MB + 64), binding.SA_ERR_INVALID_ARG),  # lse overlaps v
+    (dict(lse=A + 4 * MB + 64), binding.SA_ERR_INVALID_ARG),  # lse overlaps out
+    (dict(B=0), binding.SA_ERR_INVALID_ARG),
+    (dict(N=0), binding.SA_ERR_INVALID_ARG),
+    (dict(scale=0.0), binding.SA_ERR_INVALID_ARG),
+    (dict(scale=float("nan")), binding.SA_ERR_INVALID_ARG),
+    (dict(scale=float("inf")), binding.SA_ERR_INVALID_ARG),
+    (dict(d=96), binding.SA_ERR_UNSUPPORTED),
+    (dict(bq=64, bk=128), binding.SA_ERR_UNSUPPORTED),
+    (dict(bq=32, bk=32), binding.SA_ERR_UNSUPPORTED),
+    (dict(N=64 * 65536, bq=64, bk=64), binding.SA_ERR_UNSUPPORTED),  # n_kb > 65535
+])
+def test_fwd_rejects_bad_arguments_on_host(lib, kw, code):
+    assert _fwd(lib, **kw) == code
+
+
+def test_other_entry_points_reject_bad_arguments(lib):
+    P = ctypes.c_void_p
+    assert lib.sa_mask_prepass(None, 1, 1, 1, P(A), P(A + MB), None) == binding.SA_ERR_INVALID_ARG
+    assert lib.sa_mask_prepass(P(A), 1, 1, 70000, P(A + MB), P(A + 2 * MB), None) == \
+        binding.SA_ERR_UNSUPPORTED
+    assert lib.sa_schedule(P(A), 0, 1, 1, P(A + MB), None) == binding.SA_ERR_INVALID_ARG
+    h = P()
+    assert lib.sa_bsattn_plan_create(P(A), 1, 1, 100, 64, 128, None, ctypes.byref(h)) == \
+        binding.SA_ERR_UNSUPPORTED
+    assert h.value is None
+    assert lib.sa_bsattn_plan_create(P(A), 1, 1, 100, 64, 64, None, None) == \
+        binding.SA_ERR_INVALID_ARG
+    assert lib.sa_bsattn_fwd_plan(None, P(A), P(A), P(A), P(A), P(A), 128, ctypes.c_float(1.0),
+                                  None) == binding.SA_ERR_INVALID_ARG
+    n = ctypes.c_int64()
+    assert lib.sa_bsattn_plan_stats(None, ctypes.byref(n)) == binding.SA_ERR_INVALID_ARG
+    assert lib.sa_bsattn_plan_destroy(None) == binding.SA_ERR_INVALID_ARG

@@ -1,0 +1,100 @@
+"""Mask pre-pass and schedule through the C ABI: bit-exact against the reference."""
+
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from workloads import pack_rows
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(name):
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    if name == "random_16":
+        bm = rng.random((3, 16, 16)) < 0.3
+    elif name == "random_256":
+        bm = rng.random((4, 256, 256)) < 0.3
+    elif name == "random_591":
+        bm = rng.random((2, 591, 591)) < 0.2
+    elif name == "dense_591":
+        bm = np.ones((2, 591, 591), dtype=bool)
+    elif name == "diag_256":
+        bm = np.broadcast_to(np.eye(256, dtype=bool), (2, 256, 256)).copy()
+    elif name == "empty_rows":
+        bm = rng.random((2, 40, 40)) < 0.5
+        bm[0, 3] = False
+        bm[1, :5] = False
+    elif name == "nkb_1":
+        bm = np.ones((2, 1, 1), dtype=bool)
+    elif name == "nkb_64":
+        bm = rng.random((2, 64, 64)) < 0.5
+    elif name == "nkb_4100":   # more than 64 words per row
+        bm = rng.random((1, 3, 4100)) < 0.1
+        bm[0, 1] = True
+    else:
+        raise KeyError(name)
+    return bm
+
+
+CASES = ["random_16", "random_256", "random_591", "dense_591", "diag_256", "empty_rows", "nkb_1",
+         "nkb_64", "nkb_4100"]
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_prepass_matches_crm_walk(name):
+    from paper_2606_23019_amd import binding
+    bm = _case(name)
+    H, n_qb, n_kb = bm.shape
+    packed = pack_rows(bm)
+    counts, lists = binding.mask_prepass(packed, H, n_qb, n_kb)
+    counts = counts.cpu().numpy()
+    lists = lists.cpu().numpy().view(np.uint16).reshape(H, n_qb, n_kb)
+    for h in range(H):
+        for u in range(n_qb):
+            ref = oracle.crm_walk(packed[h, u].view("<u4"), n_kb)
+            c = int(counts[h * n_qb + u])
+            assert c == len(ref), (h, u)
+            assert lists[h, u, :c].tolist() == ref, (h, u)
+
+
+def test_prepass_ignores_bits_past_last_block():
+    from paper_2606_23019_amd import binding
+    rng = np.random.default_rng(3)
+    bm = rng.random((2, 70, 70)) < 0.4
+    packed = pack_rows(bm)
+    dirty = packed.copy()
+    dirty[:, :, -1] |= np.uint64(0xFFFF_FFFF_FFFF_FFC0)   # bits 70..127 of the row
+    c1, l1 = binding.mask_prepass(packed, 2, 70, 70)
+    c2, l2 = binding.mask_prepass(dirty, 2, 70, 70)
+    assert np.array_equal(c1.cpu().numpy(), c2.cpu().numpy())
+    n = c1.cpu().numpy()
+    a, b = l1.cpu().numpy(), l2.cpu().numpy()
+    for r in range(140):
+        assert np.array_equal(a[r, :n[r]], b[r, :n[r]])
+
+
+def test_schedule_is_a_heaviest_first_permutation():
+    from paper_2606_23019_amd import binding
+    rng = np.random.default_rng(11)
+    H, n = 7, 48
+    dens = rng.uniform(0.02, 0.9, size=H)
+    dens[3] = dens[5]                              # a tie between two heads
+    bm = np.stack([rng.random((n, n)) < p for p in dens])
+    bm[5] = bm[3]
+    for B in (1, 3):
+        packed = pack_rows(bm)
+        counts, _ = binding.mask_prepass(packed, H, n, n)
+        order = binding.schedule(counts, B, H, n).cpu().numpy()
+        assert sorted(order.tolist()) == list(range(B * H * n))
+        cost = bm.reshape(H, -1).sum(axis=1)
+        groups = order.reshape(B * H, n)
+        units = groups[:, 0] // n
+        for g, unit in zip(groups, units):
+            assert g.tolist() == [unit * n + u for u in range(n)]
+        unit_cost = [cost[unit % H] for unit in units]
+        expect = sorted(range(B * H), key=lambda x: (-cost[x % H], x))
+        assert units.tolist() == expect
+        assert all(a >= b for a, b in zip(unit_cost, unit_cost[1:]))
