@@ -223,6 +223,26 @@ def run_sweep(path, steps, warmup):
     return rows
 
 
+COPY_BYTES = 1 << 30
+
+
+def profile_run(case, steps, warmup):
+    """Launches for counter collection: the attention kernel, then a plain copy of
+    COPY_BYTES (read COPY_BYTES, write COPY_BYTES) to calibrate byte counters."""
+    import torch
+    for _ in range(warmup):
+        case.attention_only()
+    for _ in range(steps):
+        case.attention_only()
+    src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()
+    dst = torch.empty_like(src)
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_run": case.wl.name, "attention_launches": warmup + steps,
+                      "copy_launches": steps, "copy_bytes_each_way": COPY_BYTES}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -232,6 +252,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", default=None, help="also run the density/block sweep into this file")
     ap.add_argument("--configs", default=None, help="also time every named workload into this file")
+    ap.add_argument("--profile", action="store_true",
+                    help="counter-collection run: attention kernel launches plus a plain 1 GiB "
+                         "device copy (the HBM byte-counter calibration), nothing else")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -251,6 +274,9 @@ def main():
     wl = SHORT[args.workload]
     log("workload", wl.name)
     case = Case(wl)
+    if args.profile:
+        profile_run(case, args.steps, args.warmup)
+        return
     for _ in range(args.warmup):
         case.step()
     torch.cuda.synchronize()

@@ -78,11 +78,12 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v,
  * for each row r = h * n_qb + u writes counts[r] = number of set bits
  * (positions < n_kb) and lists[r * n_kb + 0 .. counts[r]-1] = the enabled key
  * blocks in ascending order.  Entries past counts[r] are left untouched.
- * counts: device int32 [H * n_qb]; lists: device uint16 [H * n_qb * n_kb].
+ * counts: device int32 [H * n_qb]; lists: device int32 [H * n_qb * n_kb]
+ * (int32 so that the attention kernel reads them with scalar loads).
  * Requires 1 <= n_kb <= 65535.
  */
 SA_API int sa_mask_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb,
-                           int32_t* counts, uint16_t* lists, void* stream);
+                           int32_t* counts, int32_t* lists, void* stream);
 
 /*
  * Work schedule (balances heads of uneven density): writes order[0 .. B*H*n_qb-1],
@@ -102,7 +103,7 @@ SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb,
  * by sa_mask_prepass and sa_schedule for the same (B, H, N, blk_q, blk_k).
  */
 SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
-                                  const int32_t* counts, const uint16_t* lists,
+                                  const int32_t* counts, const int32_t* lists,
                                   const int32_t* order, void* out, float* lse,
                                   int B, int H, int N, int d, int blk_q, int blk_k,
                                   float scale, void* stream);
@@ -112,9 +113,9 @@ SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
  * device buffers with hipMalloc, runs the pre-pass and schedule on `stream`,
  * then SYNCHRONISES `stream` to record the executed-block count.  The plan
  * keeps no pointer to mask_bits.  A plan is bound to the device that was
- * current at creation.  Plans are not thread-safe across concurrent calls on
- * different streams only in the sense that they are read-only after creation:
- * concurrent sa_bsattn_fwd_plan calls are allowed.
+ * current at creation and is read-only after creation, so concurrent
+ * sa_bsattn_fwd_plan calls (any streams) may share it; destroying it while
+ * such calls are in flight is the caller's error.
  */
 typedef struct sa_plan* sa_plan_t;
 

@@ -140,15 +140,15 @@ def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
 
 
 def mask_prepass(mask_bits, H, n_qb, n_kb, stream=None):
-    """``sa_mask_prepass``: returns (counts int32 [H*n_qb], lists int16-as-uint16 [H*n_qb, n_kb])."""
+    """``sa_mask_prepass``: returns (counts int32 [H*n_qb], lists int32 [H*n_qb, n_kb])."""
     torch = _torch()
     lib = load()
     m = mask_to_device(mask_bits)
     counts = torch.full((H * n_qb,), -1, dtype=torch.int32, device=m.device)
-    lists = torch.full((H * n_qb, n_kb), -1, dtype=torch.int16, device=m.device)
+    lists = torch.full((H * n_qb, n_kb), -1, dtype=torch.int32, device=m.device)
     st = lib.sa_mask_prepass(_dev_ptr(m, torch.int64, "mask_bits"), H, n_qb, n_kb,
                              _dev_ptr(counts, torch.int32, "counts"),
-                             _dev_ptr(lists, torch.int16, "lists"), _stream(stream))
+                             _dev_ptr(lists, torch.int32, "lists"), _stream(stream))
     _check("sa_mask_prepass", st)
     return counts, lists
 
@@ -179,7 +179,7 @@ def bsattn_fwd_prepared(q, k, v, counts, lists, order, blk_q, blk_k, scale=None,
     st = lib.sa_bsattn_fwd_prepared(
         _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
         _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(counts, torch.int32, "counts"),
-        _dev_ptr(lists, torch.int16, "lists"), _dev_ptr(order, torch.int32, "order"),
+        _dev_ptr(lists, torch.int32, "lists"), _dev_ptr(order, torch.int32, "order"),
         _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
         B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
     _check("sa_bsattn_fwd_prepared", st)

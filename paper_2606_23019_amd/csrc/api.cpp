@@ -75,7 +75,7 @@ Workspace plan_workspace(int B, int H, const Dims& dm) {
   const size_t rows = (size_t)H * dm.n_qb;
   w.counts_off = 0;
   w.lists_off = align_up(rows * 4, 256);
-  w.order_off = w.lists_off + align_up(rows * dm.n_kb * 2, 256);
+  w.order_off = w.lists_off + align_up(rows * dm.n_kb * 4, 256);
   w.total = w.order_off + align_up((size_t)B * H * dm.n_qb * 4, 256);
   return w;
 }
@@ -88,7 +88,7 @@ struct sa_plan {
   int device;
   void* buf;
   int32_t* counts;
-  uint16_t* lists;
+  int32_t* lists;
   int32_t* order;
   int64_t executed;
 };
@@ -108,9 +108,9 @@ SA_API const char* sa_status_string(int status) {
 SA_API int sa_version(void) { return kVersion; }
 
 SA_API int sa_mask_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,
-                           uint16_t* lists, void* stream) {
+                           int32_t* lists, void* stream) {
   if (!mask_bits || !counts || !lists || H < 1 || n_qb < 1 || n_kb < 1) return SA_ERR_INVALID_ARG;
-  if (!aligned(mask_bits, 8) || !aligned(counts, 4) || !aligned(lists, 2)) return SA_ERR_INVALID_ARG;
+  if (!aligned(mask_bits, 8) || !aligned(counts, 4) || !aligned(lists, 4)) return SA_ERR_INVALID_ARG;
   if (n_kb > 65535 || (int64_t)H * n_qb >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
   const hipError_t e =
       sa::launch_prepass(mask_bits, H, n_qb, n_kb, counts, lists, (hipStream_t)stream);
@@ -126,7 +126,7 @@ SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* o
 }
 
 SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
-                                  const int32_t* counts, const uint16_t* lists,
+                                  const int32_t* counts, const int32_t* lists,
                                   const int32_t* order, void* out, float* lse, int B, int H, int N,
                                   int d, int blk_q, int blk_k, float scale, void* stream) {
   Dims dm;
@@ -156,7 +156,7 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint
   if (hipMallocAsync(&ws, w.total, s) != hipSuccess || !ws) return SA_ERR_HIP;
   char* base = (char*)ws;
   int32_t* counts = (int32_t*)(base + w.counts_off);
-  uint16_t* lists = (uint16_t*)(base + w.lists_off);
+  int32_t* lists = (int32_t*)(base + w.lists_off);
   int32_t* order = (int32_t*)(base + w.order_off);
   hipError_t e = sa::launch_prepass(mask_bits, H, dm.n_qb, dm.n_kb, counts, lists, s);
   if (e == hipSuccess) e = sa::launch_schedule(counts, B, H, dm.n_qb, order, s);
@@ -186,7 +186,7 @@ SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
   if (hipMalloc(&p->buf, w.total) != hipSuccess) { delete p; return SA_ERR_HIP; }
   char* base = (char*)p->buf;
   p->counts = (int32_t*)(base + w.counts_off);
-  p->lists = (uint16_t*)(base + w.lists_off);
+  p->lists = (int32_t*)(base + w.lists_off);
   p->order = (int32_t*)(base + w.order_off);
   hipError_t e = sa::launch_prepass(mask_bits, H, dm.n_qb, dm.n_kb, p->counts, p->lists, s);
   if (e == hipSuccess) e = sa::launch_schedule(p->counts, B, H, dm.n_qb, p->order, s);

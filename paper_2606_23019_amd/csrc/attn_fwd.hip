@@ -43,18 +43,18 @@ struct Tile {
   static constexpr int kWaves = BQ / 32;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int kChunksPerRow = D / 8;  // 16-byte chunks
-  static constexpr int kChunksPerThread = BK * kChunksPerRow / kThreads;
+  // a tile is copied by wave-wide 1 KB direct-to-LDS loads (64 lanes x 16 B)
+  static constexpr int kLoadsPerWave = BK * kChunksPerRow / 64 / kWaves;
   static_assert(BQ % 32 == 0 && BK % 32 == 0 && D % 32 == 0, "tile shape");
-  static_assert((BK * kChunksPerRow) % kThreads == 0, "staging split");
+  static_assert((BK * kChunksPerRow) % (64 * kWaves) == 0, "copy split");
 };
 
-// XOR applied to the 16-byte chunk index of LDS row r.
-//  K tile: MFMA A-operand reads touch rows {0..3, 8..11} (and {4..7, 12..15})
-//  together; these XORs are distinct over each such set.
-//  V tile: a transposing read touches 4 consecutive rows x 2 chunks per
-//  16 lanes; XOR by 0, 2, 4, 6 spreads them over distinct banks.
-__device__ __forceinline__ int swz_k(int r) { return (r & 3) | ((r >> 1) & 4); }
-__device__ __forceinline__ int swz_v(int r) { return (r & 3) << 1; }
+// XOR applied to the 16-byte chunk index of LDS row r (same for K and V tiles).
+//  K reads (MFMA A operand) touch one chunk of rows {0..3, 8..11} (or
+//  {4..7, 12..15}) at a time: the XORs are 0..7, all distinct.
+//  V transposing reads touch 2 adjacent chunks (even first) of 4 consecutive
+//  rows per 16 lanes: the XORs differ in bits 1..2, so the 8 chunks are distinct.
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 3) & 1); }
 
 // Key (within a 32-key group) fed to MFMA row m: bits 2 and 3 of m swapped.
 // With this order, register i of the S^T accumulator of lane l holds key
@@ -64,38 +64,83 @@ __device__ __forceinline__ int key_of_row(int m) {
   return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
-// Copy rows key0 .. key0 + BK - 1 of a [N][D] bf16 matrix into an LDS tile,
-// 16-byte chunks XOR-swizzled per row; rows >= N are filled with zeros.
-template <typename T, int D, typename Swz>
-__device__ __forceinline__ void stage_tile(__bf16* lds, const __bf16* src, int key0, int N, int tid,
-                                           Swz swz) {
-  u32x4 r4[T::kChunksPerThread];
+// Workgroup barrier after this wave's LDS reads have completed.  Unlike
+// __syncthreads() it does not wait for outstanding global->LDS copies.  The
+// memory clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void barrier_lds_reads_done() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Workgroup barrier once all but the VM most recent global->LDS copies of
+// every wave have landed (copies complete in issue order).
+template <int VM>
+__device__ __forceinline__ void barrier_copies_landed() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(VM) : "memory");
+}
+
+// One wave-wide direct-to-LDS copy: lane l reads 16 bytes at base + voff and
+// writes them to LDS byte address m0 + 16 l.  Issued as inline assembly so
+// that the compiler does not add conservative vmcnt waits before unrelated
+// LDS reads; completion is awaited explicitly with barrier_copies_landed().
+__device__ __forceinline__ void copy16_to_lds(uint32_t lds_byte_addr, const void* base,
+                                              uint32_t voff) {
+  asm volatile("global_load_lds_dwordx4 %0, %1"
+               ::"v"(voff), "s"(base), "{m0}"(__builtin_amdgcn_readfirstlane(lds_byte_addr))
+               : "memory");
+}
+
+// Per-lane element offsets of a tile copy: lane l of load i writes the 16-byte
+// LDS chunk 64 (i + kLoadsPerWave * wave) + l, i.e. row r and physical chunk p;
+// the XOR swizzle is applied by reading source chunk p ^ swz(r).
+template <typename T, int D>
+struct CopyPlan {
+  uint32_t off[T::kLoadsPerWave];  // element offset inside a tile of D-wide rows
+  __device__ __forceinline__ void init(int wave, int lane) {
 #pragma unroll
-  for (int i = 0; i < T::kChunksPerThread; ++i) {
-    const int cidx = i * T::kThreads + tid;
-    const int r = cidx / T::kChunksPerRow;
-    const int cc = cidx % T::kChunksPerRow;
-    const int key = key0 + r;
-    r4[i] = key < N ? *(const u32x4*)(src + (int64_t)key * D + cc * 8) : u32x4{};
+    for (int i = 0; i < T::kLoadsPerWave; ++i) {
+      const int idx = (wave * T::kLoadsPerWave + i) * 64 + lane;
+      const int r = idx / T::kChunksPerRow;
+      const int p = idx % T::kChunksPerRow;
+      off[i] = (uint32_t)(r * D + ((p ^ swz(r)) << 3));
+    }
   }
+};
+
+// Start copying rows key0 .. key0 + BK - 1 of a [N][D] bf16 matrix into an
+// LDS tile with global_load_lds_dwordx4 (no registers; completion is tracked
+// by vmcnt).  In a ragged last block, rows past N repeat row N - 1: finite
+// values whose logits are masked and whose probabilities are exactly zero.
+template <typename T, int BK, int D>
+__device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, int key0, int N,
+                                                int wave_u, const CopyPlan<T, D>& cp) {
+  const __bf16* tile = src + (int64_t)key0 * D;
+  const uint32_t lds0 =
+      (uint32_t)(uintptr_t)(SA_LDS void*)lds + (uint32_t)(wave_u * T::kLoadsPerWave * 1024);
+  if (key0 + BK <= N) {
 #pragma unroll
-  for (int i = 0; i < T::kChunksPerThread; ++i) {
-    const int cidx = i * T::kThreads + tid;
-    const int r = cidx / T::kChunksPerRow;
-    const int cc = cidx % T::kChunksPerRow;
-    lds_write_b128(lds + r * D + ((cc ^ swz(r)) << 3), r4[i]);
+    for (int i = 0; i < T::kLoadsPerWave; ++i) copy16_to_lds(lds0 + i * 1024, tile, cp.off[i] * 2);
+  } else {
+    const uint32_t last = (uint32_t)(N - 1 - key0) * D;  // first element of row N - 1
+#pragma unroll
+    for (int i = 0; i < T::kLoadsPerWave; ++i) {
+      const uint32_t rbase = cp.off[i] / D * D;
+      const uint32_t o = rbase <= last ? cp.off[i] : last + (cp.off[i] - rbase);
+      copy16_to_lds(lds0 + i * 1024, tile, o * 2);
+    }
   }
 }
 
 template <int BQ, int BK, int D>
 __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const int32_t* __restrict__ counts, const uint16_t* __restrict__ lists,
+    const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
     int N, int n_qb, int n_kb, float c_log2) {
   using T = Tile<BQ, BK, D>;
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[BK * D];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[BK * D];
+  constexpr int kL = T::kLoadsPerWave;
+  __shared__ __attribute__((aligned(1024))) __bf16 Ks[BK * D];
+  __shared__ __attribute__((aligned(1024))) __bf16 Vs[BK * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -109,11 +154,20 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   const int h = bh % H;
   const int row = h * n_qb + u;
   const int cnt = counts[row];
-  const uint16_t* list = lists + (int64_t)row * n_kb;
+  const int32_t* list = lists + (int64_t)row * n_kb;
   const int64_t base = (int64_t)bh * N * D;
   const __bf16* Qb = Q + base;
   const __bf16* Kb = K + base;
   const __bf16* Vb = V + base;
+
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  CopyPlan<T, D> cp;
+  cp.init(wave_u, lane);
+  if (cnt > 0) {
+    const int key0 = list[0] * BK;
+    issue_tile_copy<T, BK, D>(Ks, Kb, key0, N, wave_u, cp);
+    issue_tile_copy<T, BK, D>(Vs, Vb, key0, N, wave_u, cp);
+  }
 
   // Q^T fragments (B operand): lane holds Q[qrow][16 dc + 8 half .. +7].
   const int qrow = u * BQ + wave * 32 + l32;
@@ -126,18 +180,25 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
       qf[dc] = bf16x8{};
   }
 
+  // Q and the first tiles have landed: the loop below starts with no
+  // outstanding vector loads that the compiler would otherwise wait for.
+  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0)
+
   f32x16 o[D / 32];
 #pragma unroll
   for (int dg = 0; dg < D / 32; ++dg) o[dg] = f32x16{};
   float m_run = -INFINITY;  // running max of the log2-domain logits
   float l_run = 0.f;        // this lane's share of the running sum
 
+  const int g = lane >> 4;
+  const int j = lane & 15;
+
   for (int t = 0; t < cnt; ++t) {
-    const int key0 = (int)list[t] * BK;
-    __syncthreads();  // previous block's LDS reads are done
-    stage_tile<T, D>(Ks, Kb, key0, N, tid, [](int r) { return swz_k(r); });
-    stage_tile<T, D>(Vs, Vb, key0, N, tid, [](int r) { return swz_v(r); });
-    __syncthreads();
+    const int key0 = list[t] * BK;
+    const bool more = t + 1 < cnt;
+    const int key1 = more ? list[t + 1] * BK : 0;
+
+    barrier_copies_landed<kL>();  // K[t] landed (V[t] may still be in flight)
 
     // S^T = K Q^T, one 32-key group per accumulator.
     f32x16 s[BK / 32];
@@ -147,10 +208,13 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
       const int kr = kg * 32 + key_of_row(l32);
 #pragma unroll
       for (int dc = 0; dc < D / 16; ++dc) {
-        const bf16x8 a = lds_read_b128(Ks + kr * D + (((2 * dc + half) ^ swz_k(kr)) << 3));
+        const bf16x8 a = lds_read_b128(Ks + kr * D + (((2 * dc + half) ^ swz(kr)) << 3));
         s[kg] = mfma32x32x16(a, qf[dc], s[kg]);
       }
     }
+
+    barrier_lds_reads_done();  // every wave is done with Ks
+    if (more) issue_tile_copy<T, BK, D>(Ks, Kb, key1, N, wave_u, cp);
 
     if (key0 + BK > N) {  // ragged last block: keys >= N do not exist
 #pragma unroll
@@ -167,9 +231,19 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     for (int kg = 0; kg < BK / 32; ++kg)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kg][i]);
-    mx = fmaxf(mx, other_half(mx));
-    const float m_new = fmaxf(m_run, mx * c_log2);
-    const float alpha = fast_exp2(m_run - m_new);
+    mx = fmaxf(mx, other_half(mx)) * c_log2;
+    // Rescale only when some row's maximum grew.  Keeping the exact running
+    // maximum (rather than a stale one) makes each row's largest probability
+    // exactly 1, which bf16 represents without error.
+    const bool grow = mx > m_run;  // always true on the first block
+    if (__any(grow)) {
+      const float m_new = grow ? mx : m_run;
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int dg = 0; dg < D / 32; ++dg) o[dg] *= alpha;
+    }
 
     bf16x8 pf[BK / 16];
     float lsum = 0.f;
@@ -179,32 +253,35 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
       for (int j8 = 0; j8 < 2; ++j8)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float p = fast_exp2(fmaf(s[kg][8 * j8 + e], c_log2, -m_new));
+          const float p = fast_exp2(fmaf(s[kg][8 * j8 + e], c_log2, -m_run));
           lsum += p;
           pf[2 * kg + j8][e] = (__bf16)p;
         }
-    l_run = l_run * alpha + lsum;
-    m_run = m_new;
-#pragma unroll
-    for (int dg = 0; dg < D / 32; ++dg) o[dg] *= alpha;
+    l_run += lsum;
+
+    if (more)
+      barrier_copies_landed<kL>();  // V[t] landed; K[t+1] may still be in flight
+    else
+      barrier_copies_landed<0>();
 
     // O^T += V^T P^T.  Lane group g = lane / 16 covers d0 = 32 dg + 16 (g & 1)
     // and keys 16 c + 8 (g >> 1) + 0..7 (two transposing reads of 4 rows).
-    const int g = lane >> 4;
-    const int j = lane & 15;
 #pragma unroll
     for (int dg = 0; dg < D / 32; ++dg) {
       const int dd = dg * 32 + 16 * (g & 1) + (j & 3) * 4;
 #pragma unroll
       for (int c = 0; c < BK / 16; ++c) {
         const int r0 = c * 16 + 8 * (g >> 1) + (j >> 2);
-        const int off = (((dd >> 3) ^ swz_v(r0)) << 3) + (dd & 7);  // same XOR for r0 + 4
+        const int off = (((dd >> 3) ^ swz(r0)) << 3) + (dd & 7);  // same XOR for r0 + 4
         const bf16x4 lo = lds_read_tr16_b64(Vs + r0 * D + off);
         const bf16x4 hi = lds_read_tr16_b64(Vs + (r0 + 4) * D + off);
         const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         o[dg] = mfma32x32x16(a, pf[c], o[dg]);
       }
     }
+
+    barrier_lds_reads_done();  // every wave is done with Vs
+    if (more) issue_tile_copy<T, BK, D>(Vs, Vb, key1, N, wave_u, cp);
   }
 
   const float l_tot = l_run + other_half(l_run);

@@ -15,7 +15,7 @@ struct AttnArgs {
   const void* k;
   const void* v;
   const int32_t* counts;
-  const uint16_t* lists;
+  const int32_t* lists;
   const int32_t* order;
   void* out;
   float* lse;
@@ -24,7 +24,7 @@ struct AttnArgs {
 };
 
 hipError_t launch_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,
-                          uint16_t* lists, hipStream_t stream);
+                          int32_t* lists, hipStream_t stream);
 
 hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* order,
                            hipStream_t stream);

@@ -27,12 +27,12 @@ constexpr int kPrepassWaves = 4;
 
 __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
     const uint64_t* __restrict__ mask, int rows, int n_kb, int W, int32_t* __restrict__ counts,
-    uint16_t* __restrict__ lists) {
+    int32_t* __restrict__ lists) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * kPrepassWaves + (threadIdx.x >> 6);
   if (row >= rows) return;  // uniform per wavefront
   const uint64_t* mrow = mask + (int64_t)row * W;
-  uint16_t* lrow = lists + (int64_t)row * n_kb;
+  int32_t* lrow = lists + (int64_t)row * n_kb;
   int done = 0;  // blocks already written for this row
   for (int w0 = 0; w0 < W; w0 += 64) {
     const int w = w0 + lane;
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
     int pos = done + incl - pc;
     while (word) {
       const int b = __builtin_ctzll(word);
-      lrow[pos++] = (uint16_t)(w * 64 + b);
+      lrow[pos++] = w * 64 + b;
       word &= word - 1ull;
     }
     done += __shfl(incl, 63, 64);
@@ -116,7 +116,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
 }  // namespace
 
 hipError_t launch_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,
-                          uint16_t* lists, hipStream_t stream) {
+                          int32_t* lists, hipStream_t stream) {
   const int rows = H * n_qb;
   const int W = (n_kb + 63) / 64;
   const int grid = (rows + kPrepassWaves - 1) / kPrepassWaves;

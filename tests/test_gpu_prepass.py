@@ -51,7 +51,7 @@ def test_prepass_matches_crm_walk(name):
     packed = pack_rows(bm)
     counts, lists = binding.mask_prepass(packed, H, n_qb, n_kb)
     counts = counts.cpu().numpy()
-    lists = lists.cpu().numpy().view(np.uint16).reshape(H, n_qb, n_kb)
+    lists = lists.cpu().numpy().reshape(H, n_qb, n_kb)
     for h in range(H):
         for u in range(n_qb):
             ref = oracle.crm_walk(packed[h, u].view("<u4"), n_kb)
