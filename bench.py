@@ -133,7 +133,7 @@ def parity_spot_check(case, n_items=4):
     return worst
 
 
-def cpu_baseline(case, budget_s=12.0, max_items=48):
+def cpu_baseline(case, budget_s=12.0):
     """The CPU reference, as it stands, on a bounded sample of the same workload."""
     import torch
     import oracle
@@ -154,7 +154,7 @@ def cpu_baseline(case, budget_s=12.0, max_items=48):
     items = [(h, int(u)) for h in heads for u in rng.permutation(wl.n_qb)]
     rng.shuffle(items)
     done_blocks, n_done, t_used = 0, 0, 0.0
-    for (h, u) in items[:max_items]:
+    for (h, u) in items:
         qb, kb, vb = host[h]
         allowed = oracle.block_mask(case.packed[h:h + 1, u:u + 1], n_kb)[0, 0]
         r0, r1 = u * wl.blk_q, min((u + 1) * wl.blk_q, wl.N)

@@ -49,12 +49,23 @@ struct Tile {
   static_assert((BK * kChunksPerRow) % (64 * kWaves) == 0, "copy split");
 };
 
-// XOR applied to the 16-byte chunk index of LDS row r (same for K and V tiles).
-//  K reads (MFMA A operand) touch one chunk of rows {0..3, 8..11} (or
-//  {4..7, 12..15}) at a time: the XORs are 0..7, all distinct.
-//  V transposing reads touch 2 adjacent chunks (even first) of 4 consecutive
-//  rows per 16 lanes: the XORs differ in bits 1..2, so the 8 chunks are distinct.
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 3) & 1); }
+// XOR applied to the 16-byte chunk index of LDS row r (same for K and V
+// tiles).  LDS is read 256 bytes (64 banks of 4 bytes) per cycle: 16 lanes of
+// a 16-byte read, or 32 lanes of an 8-byte transposing read.
+//  d = 128 (a row is one 256-byte bank line, 16 chunks): K operand reads put
+//  16 different rows at one logical chunk per cycle -> the XOR must be a
+//  bijection on r mod 16; V transposing reads put rows 4k .. 4k + 3 at 4
+//  adjacent chunks -> the XORs of those rows must differ in bits 2..3.
+//  d = 64 (two rows share a bank line, 8 chunks): the same conditions applied
+//  separately to even and odd rows.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  static_assert(D == 64 || D == 128, "head dim");
+  if constexpr (D == 128)
+    return ((r & 3) << 2) | ((r >> 2) & 3);
+  else
+    return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
 
 // Key (within a 32-key group) fed to MFMA row m: bits 2 and 3 of m swapped.
 // With this order, register i of the S^T accumulator of lane l holds key
@@ -102,7 +113,7 @@ struct CopyPlan {
       const int idx = (wave * T::kLoadsPerWave + i) * 64 + lane;
       const int r = idx / T::kChunksPerRow;
       const int p = idx % T::kChunksPerRow;
-      off[i] = (uint32_t)(r * D + ((p ^ swz(r)) << 3));
+      off[i] = (uint32_t)(r * D + ((p ^ swz<D>(r)) << 3));
     }
   }
 };
@@ -208,7 +219,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
       const int kr = kg * 32 + key_of_row(l32);
 #pragma unroll
       for (int dc = 0; dc < D / 16; ++dc) {
-        const bf16x8 a = lds_read_b128(Ks + kr * D + (((2 * dc + half) ^ swz(kr)) << 3));
+        const bf16x8 a = lds_read_b128(Ks + kr * D + (((2 * dc + half) ^ swz<D>(kr)) << 3));
         s[kg] = mfma32x32x16(a, qf[dc], s[kg]);
       }
     }
@@ -272,9 +283,9 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
 #pragma unroll
       for (int c = 0; c < BK / 16; ++c) {
         const int r0 = c * 16 + 8 * (g >> 1) + (j >> 2);
-        const int off = (((dd >> 3) ^ swz(r0)) << 3) + (dd & 7);  // same XOR for r0 + 4
-        const bf16x4 lo = lds_read_tr16_b64(Vs + r0 * D + off);
-        const bf16x4 hi = lds_read_tr16_b64(Vs + (r0 + 4) * D + off);
+        const int r1 = r0 + 4;
+        const bf16x4 lo = lds_read_tr16_b64(Vs + r0 * D + (((dd >> 3) ^ swz<D>(r0)) << 3) + (dd & 7));
+        const bf16x4 hi = lds_read_tr16_b64(Vs + r1 * D + (((dd >> 3) ^ swz<D>(r1)) << 3) + (dd & 7));
         const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         o[dg] = mfma32x32x16(a, pf[c], o[dg]);
       }
