@@ -99,7 +99,7 @@ SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb,
 /*
  * Attention kernel alone, on a pre-computed pre-pass and schedule (the
  * static-mask case: masks are built once and reused for every prompt,
- * Sec. 3 overview "Reuse for All Prompts").  counts/lists/order as produced
+ * Sec. 4 overview figure, "Reuse for All Prompts").  counts/lists/order as produced
  * by sa_mask_prepass and sa_schedule for the same (B, H, N, blk_q, blk_k).
  */
 SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,

@@ -14,7 +14,7 @@ work), written to be checked against the paper by eye:
                    CRM forward iterator (Appendix, "CRM Forward Iterator").
 * ``attention``  -- softmax attention restricted to the key blocks a query
                    block's CRM row enables (Sec. 4.3.2; mask instantiation
-                   M_p = 1[T <= p] of Sec. 3.1.2 supplies the masks).
+                   M_p = 1[T <= p] of Sec. 4.1.2 supplies the masks).
 
 Pins (tests/test_oracle_pins.py) tie every function to facts fixed by the
 paper or by mathematics: dense attention from a library routine for the

@@ -17,7 +17,7 @@ head h and query token i < N with query block u = floor(i / blk_q):
     out_i = sum_{j in K_i} exp(s_ij - lse_i) v_j
 
 Readings where the paper is silent: no causal or token-level mask (video DiTs
-use bidirectional full 3D attention, Sec. 1 and Sec. 3.1); a query with no
+use bidirectional full 3D attention, Sec. 1 and Sec. 2.1); a query with no
 allowed key gets out = 0 and lse = -inf; keys j >= N do not exist (the last
 block of a ragged sequence is short); the inputs are the exact bf16 values,
 promoted to float64 before any arithmetic.

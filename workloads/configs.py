@@ -6,7 +6,7 @@ sequence is padded to a multiple of the block size with ordinary N(0,1)
 tokens so that every block is full and FLOP counts are exact; the ragged
 lengths are separate correctness cases.  Head counts and head dimension
 (12 heads for the 1.3B model, 40 for the 14B model, d = 128) are the Wan2.1
-architectures'; the block size is the paper's B = 128 (Sec. 3.1.1, Sec. 4.3.2).
+architectures'; the block size is the paper's B = 128 (Sec. 4.1.1, Sec. 4.3.2).
 """
 
 from dataclasses import dataclass, field, replace

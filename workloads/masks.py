@@ -1,7 +1,7 @@
 """Seeded synthetic block masks shaped like the paper's static per-head masks.
 
 The paper's masks come from an offline pipeline (WEST threshold maps, FAST
-per-head thresholds, Sec. 3.1-3.2) run on Wan2.1 / HunyuanVideo weights and
+per-head thresholds, Sec. 4.1-4.2) run on Wan2.1 / HunyuanVideo weights and
 calibration prompts, none of which are available here.  These generators are
 stand-ins with the same structure: for every head a static block mask with a
 temporal window, a spatial neighbourhood, a few "global" key-block columns,
