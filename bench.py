@@ -223,6 +223,78 @@ def run_sweep(path, steps, warmup):
     return rows
 
 
+# Sequence lengths of the dense-overhead sweep (the paper's kernel comparison
+# spans 1K .. 262K tokens) and the head count used at each, chosen so that one
+# launch stays within tens of milliseconds.
+OVERHEAD_POINTS = [(1024, 40), (2048, 40), (4096, 40), (8192, 40), (16384, 40), (32768, 40),
+                   (65536, 10), (131072, 3), (262144, 1)]
+
+
+def run_overhead(path, steps, warmup):
+    """0 %-sparsity cost of the CRM machinery: the attention kernel driven by an all-ones
+    mask (and the one-shot call with pre-pass and schedule) against the maskless dense
+    path of the same kernel, with torch's SDPA as an outside reference."""
+    import torch
+    import torch.nn.functional as F
+    from paper_2606_23019_amd import binding
+    from workloads import Workload, pack_rows
+    rows = []
+    for N, H in OVERHEAD_POINTS:
+        wl = Workload(name="dense_h%d_n%d" % (H, N), B=1, H=H, N=N, d=128, blk_q=128, blk_k=128,
+                      grid=(1, 1, N), mask_kind="dense", rho=1.0)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(4000 + N)
+        q, k, v = (torch.randn((1, H, N, 128), generator=g, device="cuda").to(torch.bfloat16)
+                   for _ in range(3))
+        out = torch.empty_like(q)
+        lse = torch.empty((1, H, N), dtype=torch.float32, device="cuda")
+        n = wl.n_qb
+        mask = binding.mask_to_device(pack_rows(np.ones((H, n, n), dtype=bool)))
+        counts, lists = binding.mask_prepass(mask, H, n, n)
+        order = binding.schedule(counts, 1, H, n)
+        flops = 4.0 * H * N * N * 128
+
+        def f_dense():
+            binding.dense_attn_fwd(q, k, v, 128, wl.scale, out=out, lse=lse)
+
+        def f_kernel():
+            binding.bsattn_fwd_prepared(q, k, v, counts, lists, order, 128, 128, wl.scale,
+                                        out=out, lse=lse)
+
+        def f_oneshot():
+            binding.bsattn_fwd(q, k, v, mask, 128, 128, wl.scale, out=out, lse=lse)
+
+        def f_sdpa():
+            # fused backends only: the unfused math path would materialise N x N scores
+            from torch.nn.attention import SDPBackend, sdpa_kernel
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+                F.scaled_dot_product_attention(q, k, v, scale=wl.scale)
+        res = dict(N=N, H=H, d=128, blk=128)
+        for name, fn in (("maskless", f_dense), ("crm_kernel", f_kernel),
+                         ("crm_oneshot", f_oneshot), ("torch_sdpa", f_sdpa)):
+            try:
+                for _ in range(warmup):
+                    fn()
+                t, _ = _per_launch_time(fn, steps)
+            except RuntimeError as e:  # an SDPA backend that refuses the shape
+                log("%s at N=%d: %s" % (name, N, str(e).splitlines()[0]))
+                res[name + "_ms"] = res[name + "_tflops"] = None
+                continue
+            res[name + "_ms"] = t
+            res[name + "_tflops"] = flops / (t * 1e-3) / 1e12
+        res["overhead_kernel"] = res["crm_kernel_ms"] / res["maskless_ms"] - 1.0
+        res["overhead_oneshot"] = res["crm_oneshot_ms"] / res["maskless_ms"] - 1.0
+        res["sdpa_over_maskless"] = (res["torch_sdpa_ms"] / res["maskless_ms"]
+                                     if res["torch_sdpa_ms"] else None)
+        log(json.dumps(res))
+        rows.append(res)
+        del q, k, v, out, lse, mask, counts, lists, order
+        torch.cuda.empty_cache()
+    with open(path, "w") as f:
+        json.dump(rows, f, indent=1)
+    return rows
+
+
 COPY_BYTES = 1 << 30
 
 
@@ -252,6 +324,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", default=None, help="also run the density/block sweep into this file")
     ap.add_argument("--configs", default=None, help="also time every named workload into this file")
+    ap.add_argument("--overhead", default=None,
+                    help="also run the 0 %%-sparsity overhead sweep (1K..262K tokens) into this file")
     ap.add_argument("--profile", action="store_true",
                     help="counter-collection run: attention kernel launches plus a plain 1 GiB "
                          "device copy (the HBM byte-counter calibration), nothing else")
@@ -296,6 +370,13 @@ def main():
         dense.attention_only()
     ms_dense, _ = _per_launch_time(dense.attention_only, dense_steps)
     dense_tflops = dense.flops / (ms_dense * 1e-3) / 1e12
+
+    def maskless():
+        binding.dense_attn_fwd(case.q, case.k, case.v, wl.blk_q, wl.scale, out=dense.out,
+                               lse=dense.lse)
+    for _ in range(2):
+        maskless()
+    ms_maskless, _ = _per_launch_time(maskless, dense_steps)
     del dense
     torch.cuda.empty_cache()
 
@@ -330,6 +411,8 @@ def main():
         "dense_mask_ms": round(ms_dense, 4),
         "dense_mask_tflops": round(dense_tflops, 3),
         "speedup_vs_dense": round(ms_dense / ms_attn, 3),
+        "maskless_dense_ms": round(ms_maskless, 4),
+        "crm_overhead_at_density_1": round(ms_dense / ms_maskless - 1.0, 4),
         "parity_spot_check": parity,
         "roofline": {
             "bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
@@ -354,6 +437,8 @@ def main():
             json.dump(res, f, indent=1)
     if args.sweep:
         run_sweep(args.sweep, args.steps, args.warmup)
+    if args.overhead:
+        run_overhead(args.overhead, max(5, args.steps // 2), 2)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(rec), flush=True)

@@ -109,6 +109,19 @@ SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
                                   float scale, void* stream);
 
 /*
+ * Maskless dense attention: the same kernel with every key block enabled and
+ * no mask machinery (no pre-pass, no schedule, no workspace, no allocation).
+ * It is the 0 %-sparsity baseline against which the CRM path's overhead is
+ * measured (the paper's appendix "Detailed Kernel Overhead Analysis" compares
+ * its kernel at 0 % sparsity with a dense FlashAttention kernel).  The result
+ * equals sa_bsattn_fwd with an all-ones mask bit for bit.  blk is the tile
+ * size (64 or 128, as blk_q = blk_k above).  Arguments and errors otherwise as
+ * sa_bsattn_fwd.
+ */
+SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
+                             int B, int H, int N, int d, int blk, float scale, void* stream);
+
+/*
  * Plan API for static masks.  sa_bsattn_plan_create allocates the plan's
  * device buffers with hipMalloc, runs the pre-pass and schedule on `stream`,
  * then SYNCHRONISES `stream` to record the executed-block count.  The plan

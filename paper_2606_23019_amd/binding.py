@@ -35,6 +35,7 @@ SIGNATURES = {
     "sa_bsattn_fwd_plan": (_I, [_P, _P, _P, _P, _P, _P, _I, _F, _P]),
     "sa_bsattn_plan_stats": (_I, [_P, ctypes.POINTER(ctypes.c_int64)]),
     "sa_bsattn_plan_destroy": (_I, [_P]),
+    "sa_dense_attn_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P]),
 }
 
 
@@ -136,6 +137,25 @@ def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
         _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
         B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
     _check("sa_bsattn_fwd", st)
+    return out, lse
+
+
+def dense_attn_fwd(q, k, v, blk=128, scale=None, out=None, lse=None, stream=None):
+    """``sa_dense_attn_fwd``: maskless attention (every key block enabled)."""
+    torch = _torch()
+    lib = load()
+    B, H, N, d = q.shape
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    st = lib.sa_dense_attn_fwd(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+        _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, torch.bfloat16, "out"),
+        _dev_ptr(lse, torch.float32, "lse"), B, H, N, d, int(blk), float(scale), _stream(stream))
+    _check("sa_dense_attn_fwd", st)
     return out, lse
 
 

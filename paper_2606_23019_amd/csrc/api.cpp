@@ -169,6 +169,18 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint
   return (e == hipSuccess && ef == hipSuccess) ? SA_OK : SA_ERR_HIP;
 }
 
+SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
+                             int B, int H, int N, int d, int blk, float scale, void* stream) {
+  Dims dm;
+  int st = check_shape(B, H, N, blk, blk, &dm);
+  if (st != SA_OK) return st;
+  st = check_tensors(q, k, v, nullptr, 0, out, lse, B, H, N, d, scale);
+  if (st != SA_OK) return st;
+  sa::AttnArgs a{q, k, v, nullptr, nullptr, nullptr, out, lse, B, H, N, d, blk, blk,
+                 dm.n_qb, dm.n_kb, scale};
+  return sa::launch_attention_dense(a, (hipStream_t)stream) == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
 SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N, int blk_q,
                                  int blk_k, void* stream, sa_plan_t* plan) {
   if (!plan) return SA_ERR_INVALID_ARG;

@@ -24,6 +24,7 @@
 //      gfx950 transposing read ds_read_b64_tr_b16.
 //
 // Epilogue: out = O / l rounded to bf16, lse = (m + log2 l) ln 2.
+// The same kernel with DENSE = true is the maskless path (every key block).
 // Keys past N (ragged last block) are loaded as zeros and get -inf logits.
 
 #include <math.h>
@@ -142,7 +143,9 @@ __device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, 
   }
 }
 
-template <int BQ, int BK, int D>
+// DENSE = true is the maskless path: item i is processed by workgroup i and
+// every key block 0 .. n_kb - 1 is enabled (counts, lists and order unused).
+template <int BQ, int BK, int D, bool DENSE>
 __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
@@ -159,13 +162,15 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   const int half = lane >> 5;
   const int l32 = lane & 31;
 
-  const int item = order[blockIdx.x];
+  const int item = DENSE ? (int)blockIdx.x : order[blockIdx.x];
   const int bh = item / n_qb;
   const int u = item - bh * n_qb;
   const int h = bh % H;
   const int row = h * n_qb + u;
-  const int cnt = counts[row];
-  const int32_t* list = lists + (int64_t)row * n_kb;
+  const int cnt = DENSE ? n_kb : counts[row];
+  const int32_t* list = DENSE ? nullptr : lists + (int64_t)row * n_kb;
+  // key block of the t-th enabled block (ascending, as the CRM walk yields them)
+  auto kblk = [&](int t) { return DENSE ? t : list[t]; };
   const int64_t base = (int64_t)bh * N * D;
   const __bf16* Qb = Q + base;
   const __bf16* Kb = K + base;
@@ -175,7 +180,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   CopyPlan<T, D> cp;
   cp.init(wave_u, lane);
   if (cnt > 0) {
-    const int key0 = list[0] * BK;
+    const int key0 = kblk(0) * BK;
     issue_tile_copy<T, BK, D>(Ks, Kb, key0, N, wave_u, cp);
     issue_tile_copy<T, BK, D>(Vs, Vb, key0, N, wave_u, cp);
   }
@@ -205,9 +210,9 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   const int j = lane & 15;
 
   for (int t = 0; t < cnt; ++t) {
-    const int key0 = list[t] * BK;
+    const int key0 = kblk(t) * BK;
     const bool more = t + 1 < cnt;
-    const int key1 = more ? list[t + 1] * BK : 0;
+    const int key1 = more ? kblk(t + 1) * BK : 0;
 
     barrier_copies_landed<kL>();  // K[t] landed (V[t] may still be in flight)
 
@@ -312,27 +317,36 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   }
 }
 
-template <int BQ, int BK, int D>
+template <int BQ, int BK, int D, bool DENSE>
 hipError_t launch_tile(const AttnArgs& a, hipStream_t stream) {
   const int64_t n_items = (int64_t)a.B * a.H * a.n_qb;
-  hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D>), dim3((unsigned)n_items),
+  hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_items),
                      dim3(Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
                      (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
                      (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e);
   return hipGetLastError();
 }
 
+template <bool DENSE>
+hipError_t launch_any(const AttnArgs& a, hipStream_t stream) {
+  if (a.blk_q == 128 && a.blk_k == 128) {
+    if (a.d == 128) return launch_tile<128, 128, 128, DENSE>(a, stream);
+    if (a.d == 64) return launch_tile<128, 128, 64, DENSE>(a, stream);
+  } else if (a.blk_q == 64 && a.blk_k == 64) {
+    if (a.d == 128) return launch_tile<64, 64, 128, DENSE>(a, stream);
+    if (a.d == 64) return launch_tile<64, 64, 64, DENSE>(a, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
-  if (a.blk_q == 128 && a.blk_k == 128) {
-    if (a.d == 128) return launch_tile<128, 128, 128>(a, stream);
-    if (a.d == 64) return launch_tile<128, 128, 64>(a, stream);
-  } else if (a.blk_q == 64 && a.blk_k == 64) {
-    if (a.d == 128) return launch_tile<64, 64, 128>(a, stream);
-    if (a.d == 64) return launch_tile<64, 64, 64>(a, stream);
-  }
-  return hipErrorInvalidValue;
+  return launch_any<false>(a, stream);
+}
+
+hipError_t launch_attention_dense(const AttnArgs& a, hipStream_t stream) {
+  return launch_any<true>(a, stream);
 }
 
 }  // namespace sa

@@ -31,4 +31,7 @@ hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 
+// Maskless variant: every key block enabled; counts, lists and order unused.
+hipError_t launch_attention_dense(const AttnArgs& a, hipStream_t stream);
+
 }  // namespace sa

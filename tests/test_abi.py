@@ -91,3 +91,28 @@ def test_other_entry_points_reject_bad_arguments(lib):
     n = ctypes.c_int64()
     assert lib.sa_bsattn_plan_stats(None, ctypes.byref(n)) == binding.SA_ERR_INVALID_ARG
     assert lib.sa_bsattn_plan_destroy(None) == binding.SA_ERR_INVALID_ARG
+
+
+def _dense(lib, q=A, k=A + MB, v=A + 2 * MB, out=A + 4 * MB, lse=A + 5 * MB,
+           B=1, H=2, N=256, d=128, blk=128, scale=0.088):
+    P = ctypes.c_void_p
+    return lib.sa_dense_attn_fwd(P(q), P(k), P(v), P(out), P(lse), B, H, N, d, blk,
+                                 ctypes.c_float(scale), None)
+
+
+# every case carries at least one invalid argument: validation must stop it
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=0), binding.SA_ERR_INVALID_ARG),
+    (dict(v=0), binding.SA_ERR_INVALID_ARG),
+    (dict(out=0), binding.SA_ERR_INVALID_ARG),
+    (dict(lse=A + 5 * MB + 2), binding.SA_ERR_INVALID_ARG),   # misaligned lse
+    (dict(k=A + MB + 8), binding.SA_ERR_INVALID_ARG),         # misaligned k
+    (dict(out=A + 2 * MB + 32), binding.SA_ERR_INVALID_ARG),  # out overlaps v
+    (dict(H=0), binding.SA_ERR_INVALID_ARG),
+    (dict(scale=-1.0), binding.SA_ERR_INVALID_ARG),
+    (dict(d=32), binding.SA_ERR_UNSUPPORTED),
+    (dict(blk=256), binding.SA_ERR_UNSUPPORTED),
+    (dict(N=64 * 65536, blk=64), binding.SA_ERR_UNSUPPORTED),
+])
+def test_dense_rejects_bad_arguments_on_host(lib, kw, code):
+    assert _dense(lib, **kw) == code
