@@ -12,6 +12,8 @@ work), written to be checked against the paper by eye:
 * ``bits``       -- bf16 decoding, the Compressed Row Mask (CRM) bit layout of
                    Sec. 4.3.2 and the ascending active-block enumeration of the
                    CRM forward iterator (Appendix, "CRM Forward Iterator").
+* ``masks``      -- mask instantiation M_p = 1[T <= p] from a threshold map
+                   (Sec. 4.1.2) and CRM packing.
 * ``attention``  -- softmax attention restricted to the key blocks a query
                    block's CRM row enables (Sec. 4.3.2; mask instantiation
                    M_p = 1[T <= p] of Sec. 4.1.2 supplies the masks).
@@ -30,6 +32,7 @@ from .bits import (  # noqa: F401
     crm_walk,
     n_words_u64,
 )
+from .masks import instantiate, instantiate_packed, pack_crm  # noqa: F401
 from .attention import (  # noqa: F401
     attention_block,
     attention,
