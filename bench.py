@@ -295,6 +295,44 @@ def run_overhead(path, steps, warmup):
     return rows
 
 
+# Mask instantiation sizes: (label, H, blocks per side, thresholds per map).
+INSTANTIATE_POINTS = [("14b-480p", 40, 256, 1), ("14b-480p", 40, 256, 50),
+                      ("14b-720p", 40, 591, 1), ("14b-720p", 40, 591, 50),
+                      ("262k-tokens", 40, 2048, 1), ("262k-tokens", 40, 2048, 8)]
+
+
+def run_instantiate(path, steps, warmup):
+    """sa_mask_instantiate against its HBM roofline: T read once (4 B per block),
+    one bit per block and threshold written."""
+    import torch
+    from paper_2606_23019_amd import binding
+    rows = []
+    for label, H, n, n_p in INSTANTIATE_POINTS:
+        g = torch.Generator(device="cuda")
+        g.manual_seed(5000 + n)
+        T = torch.rand((H, n, n), generator=g, device="cuda")
+        p = torch.rand((n_p, H), generator=g, device="cuda")
+        W = (n + 63) // 64
+        out = torch.empty((n_p, H, n, W), dtype=torch.int64, device="cuda")
+
+        def fn():
+            binding.mask_instantiate(T, p, out=out)
+        for _ in range(warmup):
+            fn()
+        t, t_med = _per_launch_time(fn, steps)
+        nbytes = 4.0 * H * n * n + 8.0 * n_p * H * n * W + 4.0 * n_p * H
+        rec = dict(shape=label, H=H, n_blocks=n, n_thresholds=n_p, us=t * 1e3, us_median=t_med * 1e3,
+                   algorithmic_bytes=nbytes, gbs=nbytes / (t * 1e-3) / 1e9,
+                   frac_hbm_peak=nbytes / (t * 1e-3) / 1e9 / PEAK_HBM_GBS)
+        log(json.dumps(rec))
+        rows.append(rec)
+        del T, p, out
+        torch.cuda.empty_cache()
+    with open(path, "w") as f:
+        json.dump(rows, f, indent=1)
+    return rows
+
+
 COPY_BYTES = 1 << 30
 
 
@@ -326,6 +364,8 @@ def main():
     ap.add_argument("--configs", default=None, help="also time every named workload into this file")
     ap.add_argument("--overhead", default=None,
                     help="also run the 0 %%-sparsity overhead sweep (1K..262K tokens) into this file")
+    ap.add_argument("--instantiate", default=None,
+                    help="also time mask instantiation from threshold maps into this file")
     ap.add_argument("--profile", action="store_true",
                     help="counter-collection run: attention kernel launches plus a plain 1 GiB "
                          "device copy (the HBM byte-counter calibration), nothing else")
@@ -439,6 +479,8 @@ def main():
         run_sweep(args.sweep, args.steps, args.warmup)
     if args.overhead:
         run_overhead(args.overhead, max(5, args.steps // 2), 2)
+    if args.instantiate:
+        run_instantiate(args.instantiate, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(rec), flush=True)

@@ -86,6 +86,23 @@ SA_API int sa_mask_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb,
                            int32_t* counts, int32_t* lists, void* stream);
 
 /*
+ * Mask instantiation from a threshold map (Sec. 4.1.2, Eq. 2 and the mask
+ * M_p = 1[T <= p] that follows it): WEST's map T holds, per head and block,
+ * the smallest density threshold at which the block is active; FAST chooses
+ * a threshold per layer, timestep and head (Sec. 4.2.2).  For every
+ * threshold set i and head h this writes the CRM row bits
+ *   bit (v mod 64) of mask_bits[i][h][u][v / 64] = 1[T[h][u][v] <= p[i][h]]
+ * with bits past n_kb zero; a NaN in T or p leaves the block off.  The
+ * output of set i is exactly the mask_bits argument of sa_bsattn_fwd.
+ * T: device float32 [H][n_qb][n_kb]; p: device float32 [n_p][H];
+ * mask_bits: device uint64 [n_p][H][n_qb][W], W = ceil(n_kb / 64), every word
+ * written.  mask_bits must not overlap T or p.  Requires n_p, H, n_qb >= 1
+ * and 1 <= n_kb <= 65535.
+ */
+SA_API int sa_mask_instantiate(const float* T, const float* p, int n_p, int H, int n_qb, int n_kb,
+                               uint64_t* mask_bits, void* stream);
+
+/*
  * Work schedule (balances heads of uneven density): writes order[0 .. B*H*n_qb-1],
  * a permutation of the work items it = (b * H + h) * n_qb + u.  Items of one
  * (b, h) stay together in ascending u; (b, h) groups are ordered by

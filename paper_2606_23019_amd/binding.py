@@ -36,6 +36,7 @@ SIGNATURES = {
     "sa_bsattn_plan_stats": (_I, [_P, ctypes.POINTER(ctypes.c_int64)]),
     "sa_bsattn_plan_destroy": (_I, [_P]),
     "sa_dense_attn_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P]),
+    "sa_mask_instantiate": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
 }
 
 
@@ -157,6 +158,28 @@ def dense_attn_fwd(q, k, v, blk=128, scale=None, out=None, lse=None, stream=None
         _dev_ptr(lse, torch.float32, "lse"), B, H, N, d, int(blk), float(scale), _stream(stream))
     _check("sa_dense_attn_fwd", st)
     return out, lse
+
+
+def mask_instantiate(T, p, out=None, stream=None):
+    """``sa_mask_instantiate``: CRM masks 1[T <= p] for every threshold set.
+
+    T: float32 device tensor [H, n_qb, n_kb]; p: float32 device tensor [n_p, H].
+    Returns int64 (uint64 bits) [n_p, H, n_qb, W].
+    """
+    torch = _torch()
+    lib = load()
+    H, n_qb, n_kb = T.shape
+    n_p = p.shape[0]
+    if tuple(p.shape) != (n_p, H):
+        raise ValueError("p must be [n_p, H]")
+    W = (n_kb + 63) // 64
+    if out is None:
+        out = torch.empty((n_p, H, n_qb, W), dtype=torch.int64, device=T.device)
+    st = lib.sa_mask_instantiate(_dev_ptr(T, torch.float32, "T"), _dev_ptr(p, torch.float32, "p"),
+                                 n_p, H, n_qb, n_kb, _dev_ptr(out, torch.int64, "mask_bits"),
+                                 _stream(stream))
+    _check("sa_mask_instantiate", st)
+    return out
 
 
 def mask_prepass(mask_bits, H, n_qb, n_kb, stream=None):

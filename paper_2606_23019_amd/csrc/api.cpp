@@ -117,6 +117,25 @@ SA_API int sa_mask_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb,
   return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
+SA_API int sa_mask_instantiate(const float* T, const float* p, int n_p, int H, int n_qb, int n_kb,
+                               uint64_t* mask_bits, void* stream) {
+  if (!T || !p || !mask_bits || n_p < 1 || H < 1 || n_qb < 1 || n_kb < 1) return SA_ERR_INVALID_ARG;
+  if (!aligned(T, 4) || !aligned(p, 4) || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
+  if (n_kb > 65535) return SA_ERR_UNSUPPORTED;
+  const int64_t rows = (int64_t)H * n_qb;
+  const int64_t W = (n_kb + 63) / 64;
+  if (rows >= ((int64_t)1 << 31) || (int64_t)n_p * rows * W >= ((int64_t)1 << 40))
+    return SA_ERR_UNSUPPORTED;
+  const size_t t_bytes = (size_t)rows * n_kb * 4;
+  const size_t p_bytes = (size_t)n_p * H * 4;
+  const size_t b_bytes = (size_t)n_p * rows * W * 8;
+  if (overlap(mask_bits, b_bytes, T, t_bytes) || overlap(mask_bits, b_bytes, p, p_bytes))
+    return SA_ERR_INVALID_ARG;
+  const hipError_t e =
+      sa::launch_mask_instantiate(T, p, n_p, H, n_qb, n_kb, mask_bits, (hipStream_t)stream);
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
 SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* order, void* stream) {
   if (!counts || !order || B < 1 || H < 1 || n_qb < 1) return SA_ERR_INVALID_ARG;
   if (!aligned(counts, 4) || !aligned(order, 4)) return SA_ERR_INVALID_ARG;

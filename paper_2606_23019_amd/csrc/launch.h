@@ -29,6 +29,9 @@ hipError_t launch_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, 
 hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* order,
                            hipStream_t stream);
 
+hipError_t launch_mask_instantiate(const float* T, const float* p, int n_p, int H, int n_qb,
+                                   int n_kb, uint64_t* bits, hipStream_t stream);
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 
 // Maskless variant: every key block enabled; counts, lists and order unused.

@@ -1,0 +1,73 @@
+// Mask instantiation from a threshold map (paper Sec. 4.1.2): the mask for a
+// density threshold p is M_p = 1[T <= p], one comparison per block, stored in
+// the CRM layout (LSB-first uint64 words per query-block row).
+//
+// One wavefront per row (h, u), eight words at a time.  Lane l loads
+// T[h][u][64 w + l] for the eight words of the group into registers (all loads
+// in flight together); then for every threshold p[i][h] a wavefront ballot of
+// the comparison is the word itself (ballot bit l is lane l's predicate, i.e.
+// key block 64 w + l at bit l), lane k keeps word k, and the
+// group's words leave in one 64-byte store.  The map is read from memory once
+// for all thresholds (a head's map serves every timestep of its layer): 4 bytes
+// read per block, one bit written per block and threshold, three vector
+// instructions per 64 bits.
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace sa {
+
+namespace {
+
+constexpr int kInstWaves = 4;
+constexpr int kGroup = 8;  // words whose map entries a lane holds in registers at once
+
+__global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
+    const float* __restrict__ T, const float* __restrict__ p, int n_p, int H, int n_qb, int n_kb,
+    int W, uint64_t* __restrict__ bits) {
+  const int lane = threadIdx.x & 63;
+  const int64_t rows = (int64_t)H * n_qb;
+  const int64_t row = (int64_t)blockIdx.x * kInstWaves + (threadIdx.x >> 6);
+  if (row >= rows) return;  // uniform per wavefront
+  const int h = (int)(row / n_qb);
+  const float* trow = T + row * n_kb;
+  for (int w0 = 0; w0 < W; w0 += kGroup) {
+    const int nw = min(kGroup, W - w0);
+    // all loads of the group first (independent, in flight together)
+    float t[kGroup];
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) {
+      const int v = (w0 + k) * 64 + lane;
+      t[k] = (k < nw && v < n_kb) ? trow[v] : __builtin_nanf("");  // NaN: never on
+    }
+    for (int i = 0; i < n_p; ++i) {
+      const float pi = p[(int64_t)i * H + h];
+      uint32_t lo = 0, hi = 0;  // lane k ends up holding word w0 + k
+#pragma unroll
+      for (int k = 0; k < kGroup; ++k) {
+        if (k < nw) {  // uniform
+          const uint64_t word = __ballot(t[k] <= pi);
+          if (lane == k) {
+            lo = (uint32_t)word;
+            hi = (uint32_t)(word >> 32);
+          }
+        }
+      }
+      if (lane < nw) bits[((int64_t)i * rows + row) * W + w0 + lane] = ((uint64_t)hi << 32) | lo;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_mask_instantiate(const float* T, const float* p, int n_p, int H, int n_qb,
+                                   int n_kb, uint64_t* bits, hipStream_t stream) {
+  const int64_t rows = (int64_t)H * n_qb;
+  const int W = (n_kb + 63) / 64;
+  const int64_t grid = (rows + kInstWaves - 1) / kInstWaves;
+  hipLaunchKernelGGL(mask_inst_kernel, dim3((unsigned)grid), dim3(64 * kInstWaves), 0, stream, T, p,
+                     n_p, H, n_qb, n_kb, W, bits);
+  return hipGetLastError();
+}
+
+}  // namespace sa

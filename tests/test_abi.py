@@ -116,3 +116,26 @@ def _dense(lib, q=A, k=A + MB, v=A + 2 * MB, out=A + 4 * MB, lse=A + 5 * MB,
 ])
 def test_dense_rejects_bad_arguments_on_host(lib, kw, code):
     assert _dense(lib, **kw) == code
+
+
+def _inst(lib, T=A, p=A + MB, n_p=2, H=3, n_qb=4, n_kb=100, bits=A + 2 * MB):
+    P = ctypes.c_void_p
+    return lib.sa_mask_instantiate(P(T), P(p), n_p, H, n_qb, n_kb, P(bits), None)
+
+
+# every case carries at least one invalid argument: validation must stop it
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=0), binding.SA_ERR_INVALID_ARG),
+    (dict(p=0), binding.SA_ERR_INVALID_ARG),
+    (dict(bits=0), binding.SA_ERR_INVALID_ARG),
+    (dict(T=A + 2), binding.SA_ERR_INVALID_ARG),          # misaligned map
+    (dict(bits=A + 2 * MB + 4), binding.SA_ERR_INVALID_ARG),  # misaligned words
+    (dict(bits=A + 64), binding.SA_ERR_INVALID_ARG),      # output overlaps the map
+    (dict(bits=A + MB - 8), binding.SA_ERR_INVALID_ARG),  # output runs into p
+    (dict(n_p=0), binding.SA_ERR_INVALID_ARG),
+    (dict(H=0), binding.SA_ERR_INVALID_ARG),
+    (dict(n_kb=0), binding.SA_ERR_INVALID_ARG),
+    (dict(n_kb=65536), binding.SA_ERR_UNSUPPORTED),
+])
+def test_instantiate_rejects_bad_arguments_on_host(lib, kw, code):
+    assert _inst(lib, **kw) == code
