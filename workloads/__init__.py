@@ -11,4 +11,4 @@ from .configs import (  # noqa: F401
 )
 from .masks import make_masks, pack_rows, structured_head, uniform_head, block_centres  # noqa: F401
 from .tensors import head_scales, masks_for, qkv_for, bf16_to_bits, sample_items  # noqa: F401
-from .thresholds import threshold_maps, p_for_density  # noqa: F401
+from .thresholds import threshold_maps, p_for_density, stratified_rows  # noqa: F401

@@ -52,3 +52,28 @@ def p_for_density(T, rho):
     rho = np.broadcast_to(np.asarray(rho, dtype=np.float64), (H,))
     idx = np.clip(np.ceil(rho * n).astype(np.int64) - 1, 0, n - 1)
     return flat[np.arange(H), idx].astype(np.float32)
+
+
+def stratified_rows(N, H, n_strata=16, per_stratum=1, seed=0):
+    """Sampled query rows per head for fidelity profiling (paper Sec. 4.2.3).
+
+    The N rows are cut into ``n_strata`` equal strata and ``per_stratum`` rows
+    are drawn uniformly (without replacement) from each, so every part of the
+    sequence is represented.  The paper profiles with 16 rows, about 0.05 % of
+    a 32K-token map; read here as 16 strata of one row each.  Returns int32
+    ``[H][n_strata * per_stratum]``, ascending per head.
+    """
+    rng = np.random.default_rng(seed)
+    edges = np.linspace(0, N, n_strata + 1).astype(np.int64)
+    out = np.empty((H, n_strata * per_stratum), dtype=np.int32)
+    for h in range(H):
+        picks = []
+        for s in range(n_strata):
+            lo, hi = int(edges[s]), int(edges[s + 1])
+            n = max(hi - lo, 1)
+            take = min(per_stratum, n)
+            sel = rng.choice(n, size=take, replace=False) + lo
+            sel = np.pad(sel, (0, per_stratum - take), mode="edge")
+            picks.append(np.sort(sel))
+        out[h] = np.minimum(np.concatenate(picks), N - 1)
+    return out
