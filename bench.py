@@ -333,6 +333,49 @@ def run_instantiate(path, steps, warmup):
     return rows
 
 
+# Fidelity profiling sizes: (workload, sampled rows per head, candidate thresholds).
+FIDELITY_POINTS = [("14b-480p", 16, 16), ("14b-720p", 16, 16), ("14b-720p", 32, 64)]
+
+
+def run_fidelity(path, steps, warmup):
+    """sa_fidelity_profile against its HBM roofline: every head's K is read once
+    (B H N d 2 bytes); the sampled rows' Q, the block log-masses (written, then
+    read), the rows' threshold-map rows and the outputs are small beside it."""
+    import torch
+    from paper_2606_23019_amd import binding
+    from workloads import SHORT, qkv_for, stratified_rows, threshold_maps
+    rows_out = []
+    for name, R, K in FIDELITY_POINTS:
+        wl = SHORT[name]
+        q, k, v = qkv_for(wl, device="cuda")
+        del v
+        T = torch.from_numpy(threshold_maps(wl.H, wl.n_qb, wl.n_kb, wl.blk_q, wl.grid,
+                                            seed=wl.mask_seed)).cuda()
+        rows = torch.from_numpy(stratified_rows(wl.N, wl.H, n_strata=R, seed=wl.sample_seed)).cuda()
+        p = torch.linspace(0.0, 1.0, K, device="cuda")
+
+        def fn():
+            binding.fidelity_profile(q, k, rows, T, p, wl.blk_q, wl.scale)
+        for _ in range(warmup):
+            fn()
+        t, t_med = _per_launch_time(fn, steps)
+        BH = wl.B * wl.H
+        nbytes = (2.0 * BH * wl.N * wl.d + 2.0 * BH * R * wl.d + 2 * 4.0 * BH * R * wl.n_kb
+                  + 4.0 * wl.H * R * wl.n_kb + 4.0 * BH * R * K + 4.0 * BH * K)
+        flops = 2.0 * BH * wl.N * 32 * wl.d   # MFMA work incl. the padding of R to 32 columns
+        rec = dict(workload=wl.name, rows_per_head=R, candidates=K, ms=t, ms_median=t_med,
+                   algorithmic_bytes=nbytes, gbs=nbytes / (t * 1e-3) / 1e9,
+                   frac_hbm_peak=nbytes / (t * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                   mfma_tflops=flops / (t * 1e-3) / 1e12)
+        log(json.dumps(rec))
+        rows_out.append(rec)
+        del q, k, T, rows, p
+        torch.cuda.empty_cache()
+    with open(path, "w") as f:
+        json.dump(rows_out, f, indent=1)
+    return rows_out
+
+
 COPY_BYTES = 1 << 30
 
 
@@ -366,6 +409,8 @@ def main():
                     help="also run the 0 %%-sparsity overhead sweep (1K..262K tokens) into this file")
     ap.add_argument("--instantiate", default=None,
                     help="also time mask instantiation from threshold maps into this file")
+    ap.add_argument("--fidelity", default=None,
+                    help="also time the Hellinger fidelity profile into this file")
     ap.add_argument("--profile", action="store_true",
                     help="counter-collection run: attention kernel launches plus a plain 1 GiB "
                          "device copy (the HBM byte-counter calibration), nothing else")
@@ -481,6 +526,8 @@ def main():
         run_overhead(args.overhead, max(5, args.steps // 2), 2)
     if args.instantiate:
         run_instantiate(args.instantiate, args.steps, args.warmup)
+    if args.fidelity:
+        run_fidelity(args.fidelity, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(rec), flush=True)

@@ -139,6 +139,29 @@ SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* 
                              int B, int H, int N, int d, int blk, float scale, void* stream);
 
 /*
+ * Fidelity profile of threshold-map masks on sampled query rows (FAST's
+ * offline profiling: Hellinger distance Sec. 4.2.1 Eq. 3, Fidelity Score
+ * Eq. 4, stratified row sampling Sec. 4.2.3).  For batch b, head h, sampled
+ * row i (query token r = rows[h][i], query block u = r / blk) and candidate
+ * threshold p[c], with P the dense softmax row of token r over all N keys and
+ * P~ the softmax over the keys of the blocks v with T[h][u][v] <= p[c] (zero
+ * elsewhere):
+ *   hellinger[b][h][i][c] = H(P, P~)                 (1 if no block is kept)
+ *   fidelity[b][h][c]     = 1 - mean_i hellinger[b][h][i][c]
+ *   blk_lse[b][h][i][v]   = log sum_{j in block v} exp(scale <q_r, k_j>)
+ * (blk_lse is also the working buffer between the two kernels.)
+ * q, k: bf16 [B][H][N][d] as above; rows: device int32 [H][R], entries
+ * clamped to [0, N); T: device float32 [H][n_qb][n_kb] (n_qb = n_kb =
+ * ceil(N / blk)); p: device float32 [K]; outputs float32 as shown.  Outputs
+ * must not overlap inputs or each other.  Requires 1 <= R <= 32,
+ * 1 <= K <= 64, B * H <= 65535, d in {64, 128}, blk in {64, 128}.
+ */
+SA_API int sa_fidelity_profile(const void* q, const void* k, const int32_t* rows, int R,
+                               const float* T, const float* p, int K, float* blk_lse,
+                               float* hellinger, float* fidelity, int B, int H, int N, int d,
+                               int blk, float scale, void* stream);
+
+/*
  * Plan API for static masks.  sa_bsattn_plan_create allocates the plan's
  * device buffers with hipMalloc, runs the pre-pass and schedule on `stream`,
  * then SYNCHRONISES `stream` to record the executed-block count.  The plan

@@ -45,23 +45,31 @@ def fidelity_score(P, Q):
     return 1.0 - hellinger(P, Q)
 
 
+def _softmax_over(s, allowed=None):
+    """Softmax of logits s over the allowed positions (all if None), zero elsewhere."""
+    if allowed is None:
+        allowed = np.ones(s.shape, dtype=bool)
+    if not allowed.any():
+        return None
+    t = np.where(allowed, s, -np.inf)
+    t = t - t[allowed].max()
+    e = np.where(allowed, np.exp(t), 0.0)
+    return e / e.sum()
+
+
+def logits(q_row, k, scale):
+    """s_j = scale * <q, k_j> for every key j (float64)."""
+    return scale * (_f64(k) @ _f64(q_row))
+
+
 def dense_row(q_row, k, scale):
     """Dense softmax row of one query over all keys (float64)."""
-    s = scale * (_f64(k) @ _f64(q_row))
-    s = s - s.max()
-    e = np.exp(s)
-    return e / e.sum()
+    return _softmax_over(logits(q_row, k, scale))
 
 
 def sparse_row(q_row, k, allowed_keys, scale):
     """Softmax restricted to the allowed keys, zero elsewhere; None if nothing is allowed."""
-    if not allowed_keys.any():
-        return None
-    s = scale * (_f64(k) @ _f64(q_row))
-    s = np.where(allowed_keys, s, -np.inf)
-    s = s - s[allowed_keys].max()
-    e = np.where(allowed_keys, np.exp(s), 0.0)
-    return e / e.sum()
+    return _softmax_over(logits(q_row, k, scale), allowed_keys)
 
 
 def profile(q, k, rows, T, p_cands, blk, scale):
@@ -70,6 +78,9 @@ def profile(q, k, rows, T, p_cands, blk, scale):
     q, k: [B][H][N][d] (bf16 bit patterns or floats); rows: int [H][R] query
     token indices per head (shared by the batch); T: [H][n_qb][n_kb] map;
     p_cands: [K] candidate thresholds.  Returns (Hd [B][H][R][K], F [B][H][K]).
+    A row's logits do not depend on the candidate, so they are formed once per
+    row; each candidate then restricts and renormalises them (P~) and Eq. 3 is
+    taken against the dense row P.
     """
     q = np.asarray(q)
     k = np.asarray(k)
@@ -83,12 +94,33 @@ def profile(q, k, rows, T, p_cands, blk, scale):
     Hd = np.zeros((B, H, R, K))
     for b in range(B):
         for h in range(H):
+            kf = _f64(k[b, h])
             for i in range(R):
                 r = int(rows[h, i])
-                P = dense_row(q[b, h, r], k[b, h], scale)
+                s = scale * (kf @ _f64(q[b, h, r]))
+                P = _softmax_over(s)
                 u = r // blk
                 for c in range(K):
                     on_blocks = T[h, u] <= p_cands[c]
-                    Qs = sparse_row(q[b, h, r], k[b, h], on_blocks[key_block], scale)
+                    Qs = _softmax_over(s, on_blocks[key_block])
                     Hd[b, h, i, c] = 1.0 if Qs is None else hellinger(P, Qs)
     return Hd, 1.0 - Hd.mean(axis=2)
+
+
+def block_log_mass(q_row, k, blk, scale):
+    """log sum_{j in block v} exp(s_j) for every key block v (natural log, float64).
+
+    The per-block pooled attention mass of one query row before normalisation:
+    exp(block_log_mass - logsumexp over all keys) is the probability mass the
+    dense row puts on block v (the row-sampled form of the block pooling of
+    Sec. 4.1.1, Eq. 1, summed instead of averaged).
+    """
+    s = logits(q_row, k, scale)
+    N = s.shape[0]
+    n_kb = -(-N // blk)
+    out = np.empty(n_kb)
+    for v in range(n_kb):
+        sv = s[v * blk:min((v + 1) * blk, N)]
+        mx = sv.max()
+        out[v] = mx + np.log(np.exp(sv - mx).sum())
+    return out

@@ -37,6 +37,8 @@ SIGNATURES = {
     "sa_bsattn_plan_destroy": (_I, [_P]),
     "sa_dense_attn_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P]),
     "sa_mask_instantiate": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
+    "sa_fidelity_profile": (_I, [_P, _P, _P, _I, _P, _P, _I, _P, _P, _P, _I, _I, _I, _I, _I, _F,
+                                 _P]),
 }
 
 
@@ -180,6 +182,33 @@ def mask_instantiate(T, p, out=None, stream=None):
                                  _stream(stream))
     _check("sa_mask_instantiate", st)
     return out
+
+
+def fidelity_profile(q, k, rows, T, p, blk, scale=None, stream=None):
+    """``sa_fidelity_profile``: returns (hellinger [B,H,R,K], fidelity [B,H,K], blk_lse [B,H,R,n_kb]).
+
+    rows: int32 device tensor [H, R]; T: float32 device [H, n_qb, n_kb]; p: float32 device [K].
+    """
+    torch = _torch()
+    lib = load()
+    B, H, N, d = q.shape
+    R = rows.shape[1]
+    K = p.shape[0]
+    n_kb = (N + blk - 1) // blk
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    dev = q.device
+    blk_lse = torch.empty((B, H, R, n_kb), dtype=torch.float32, device=dev)
+    hel = torch.empty((B, H, R, K), dtype=torch.float32, device=dev)
+    fid = torch.empty((B, H, K), dtype=torch.float32, device=dev)
+    st = lib.sa_fidelity_profile(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+        _dev_ptr(rows, torch.int32, "rows"), R, _dev_ptr(T, torch.float32, "T"),
+        _dev_ptr(p, torch.float32, "p"), K, _dev_ptr(blk_lse, torch.float32, "blk_lse"),
+        _dev_ptr(hel, torch.float32, "hellinger"), _dev_ptr(fid, torch.float32, "fidelity"),
+        B, H, N, d, int(blk), float(scale), _stream(stream))
+    _check("sa_fidelity_profile", st)
+    return hel, fid, blk_lse
 
 
 def mask_prepass(mask_bits, H, n_qb, n_kb, stream=None):

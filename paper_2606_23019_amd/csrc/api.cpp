@@ -200,6 +200,43 @@ SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* 
   return sa::launch_attention_dense(a, (hipStream_t)stream) == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
+SA_API int sa_fidelity_profile(const void* q, const void* k, const int32_t* rows, int R,
+                               const float* T, const float* p, int K, float* blk_lse,
+                               float* hellinger, float* fidelity, int B, int H, int N, int d,
+                               int blk, float scale, void* stream) {
+  Dims dm;
+  int st = check_shape(B, H, N, blk, blk, &dm);
+  if (st != SA_OK) return st;
+  if (d != 64 && d != 128) return SA_ERR_UNSUPPORTED;
+  if (!(scale > 0.f) || !isfinite(scale)) return SA_ERR_INVALID_ARG;
+  if (!q || !k || !rows || !T || !p || !blk_lse || !hellinger || !fidelity) return SA_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(rows, 4) || !aligned(T, 4) ||
+      !aligned(p, 4) || !aligned(blk_lse, 4) || !aligned(hellinger, 4) || !aligned(fidelity, 4))
+    return SA_ERR_INVALID_ARG;
+  if (R < 1 || K < 1) return SA_ERR_INVALID_ARG;
+  if (!sa::fidelity_supported(R, K) || (int64_t)B * H > 65535) return SA_ERR_UNSUPPORTED;
+  const size_t tensor_bytes = (size_t)B * H * N * d * 2;
+  const size_t rows_bytes = (size_t)H * R * 4;
+  const size_t t_bytes = (size_t)H * dm.n_qb * dm.n_kb * 4;
+  const size_t p_bytes = (size_t)K * 4;
+  const size_t lse_bytes = (size_t)B * H * R * dm.n_kb * 4;
+  const size_t hel_bytes = (size_t)B * H * R * K * 4;
+  const size_t fid_bytes = (size_t)B * H * K * 4;
+  const void* ins[5] = {q, k, rows, T, p};
+  const size_t in_bytes[5] = {tensor_bytes, tensor_bytes, rows_bytes, t_bytes, p_bytes};
+  const void* outs[3] = {blk_lse, hellinger, fidelity};
+  const size_t out_bytes[3] = {lse_bytes, hel_bytes, fid_bytes};
+  for (int o = 0; o < 3; ++o) {
+    for (int i = 0; i < 5; ++i)
+      if (overlap(outs[o], out_bytes[o], ins[i], in_bytes[i])) return SA_ERR_INVALID_ARG;
+    for (int o2 = o + 1; o2 < 3; ++o2)
+      if (overlap(outs[o], out_bytes[o], outs[o2], out_bytes[o2])) return SA_ERR_INVALID_ARG;
+  }
+  const hipError_t e = sa::launch_fidelity(q, k, rows, R, T, p, K, blk_lse, hellinger, fidelity, B,
+                                           H, N, d, blk, scale, (hipStream_t)stream);
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
 SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N, int blk_q,
                                  int blk_k, void* stream, sa_plan_t* plan) {
   if (!plan) return SA_ERR_INVALID_ARG;

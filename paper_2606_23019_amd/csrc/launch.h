@@ -32,6 +32,12 @@ hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_
 hipError_t launch_mask_instantiate(const float* T, const float* p, int n_p, int H, int n_qb,
                                    int n_kb, uint64_t* bits, hipStream_t stream);
 
+bool fidelity_supported(int R, int K);
+
+hipError_t launch_fidelity(const void* q, const void* k, const int32_t* rows, int R, const float* T,
+                           const float* p, int K, float* blk_lse, float* hel, float* fid, int B,
+                           int H, int N, int d, int blk, float scale, hipStream_t stream);
+
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream);
 
 // Maskless variant: every key block enabled; counts, lists and order unused.

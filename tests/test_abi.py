@@ -139,3 +139,34 @@ def _inst(lib, T=A, p=A + MB, n_p=2, H=3, n_qb=4, n_kb=100, bits=A + 2 * MB):
 ])
 def test_instantiate_rejects_bad_arguments_on_host(lib, kw, code):
     assert _inst(lib, **kw) == code
+
+
+def _fid(lib, q=A, k=A + MB, rows=A + 2 * MB, R=16, T=A + 3 * MB, p=A + 4 * MB, K=8,
+         lse=A + 5 * MB, hel=A + 6 * MB, fid=A + 7 * MB, B=1, H=2, N=1000, d=128, blk=128,
+         scale=0.088):
+    P = ctypes.c_void_p
+    return lib.sa_fidelity_profile(P(q), P(k), P(rows), R, P(T), P(p), K, P(lse), P(hel), P(fid),
+                                   B, H, N, d, blk, ctypes.c_float(scale), None)
+
+
+# every case carries at least one invalid argument: validation must stop it
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=0), binding.SA_ERR_INVALID_ARG),
+    (dict(rows=0), binding.SA_ERR_INVALID_ARG),
+    (dict(T=0), binding.SA_ERR_INVALID_ARG),
+    (dict(fid=0), binding.SA_ERR_INVALID_ARG),
+    (dict(k=A + MB + 8), binding.SA_ERR_INVALID_ARG),        # misaligned k
+    (dict(hel=A + 6 * MB + 2), binding.SA_ERR_INVALID_ARG),  # misaligned output
+    (dict(lse=A + 3 * MB + 16), binding.SA_ERR_INVALID_ARG),  # blk_lse overlaps T
+    (dict(hel=A + 5 * MB + 64), binding.SA_ERR_INVALID_ARG),  # outputs overlap
+    (dict(R=0), binding.SA_ERR_INVALID_ARG),
+    (dict(K=0), binding.SA_ERR_INVALID_ARG),
+    (dict(scale=0.0), binding.SA_ERR_INVALID_ARG),
+    (dict(R=33), binding.SA_ERR_UNSUPPORTED),
+    (dict(K=65), binding.SA_ERR_UNSUPPORTED),
+    (dict(B=2, H=40000), binding.SA_ERR_UNSUPPORTED),
+    (dict(d=96), binding.SA_ERR_UNSUPPORTED),
+    (dict(blk=32), binding.SA_ERR_UNSUPPORTED),
+])
+def test_fidelity_rejects_bad_arguments_on_host(lib, kw, code):
+    assert _fid(lib, **kw) == code

@@ -136,16 +136,18 @@ def _hel_squared(P, Q):
 
 
 def _prof_unnormalised(q, k, rows, T, p, blk, scale):
-    orig = ofid.sparse_row
+    orig = ofid._softmax_over
 
-    def unnorm(q_row, kk, allowed, sc):
-        r = orig(q_row, kk, np.ones_like(allowed), sc)
-        return np.where(allowed, r, 0.0) if allowed.any() else None
-    ofid.sparse_row = unnorm
+    def unnorm(s, allowed=None):
+        full = orig(s)
+        if allowed is None:
+            return full
+        return np.where(allowed, full, 0.0) if allowed.any() else None
+    ofid._softmax_over = unnorm
     try:
         return ofid.profile(q, k, rows, T, p, blk, scale)
     finally:
-        ofid.sparse_row = orig
+        ofid._softmax_over = orig
 
 
 def _prof_strict(q, k, rows, T, p, blk, scale):
@@ -185,3 +187,16 @@ def test_planted_mistakes_are_caught(name):
         if not ok:
             failed.append(pin.__name__)
     assert failed, "planted mistake %s passed every pin" % name
+
+
+def test_block_log_mass_sums_to_dense_row_blocks():
+    rng = np.random.default_rng(9)
+    q_row, k = rng.normal(size=8), rng.normal(size=(70, 8))
+    blm = ofid.block_log_mass(q_row, k, 16, 0.5)
+    P = ofid.dense_row(q_row, k, 0.5)
+    total = np.log(np.exp(blm - blm.max()).sum()) + blm.max()
+    masses = np.exp(blm - total)
+    ref = np.array([P[v * 16:(v + 1) * 16].sum() for v in range(5)])   # last block holds 6 keys
+    assert np.allclose(masses, ref, atol=1e-15) and abs(masses.sum() - 1.0) < 1e-14
+    s = 0.5 * (k @ q_row)
+    assert abs(total - math.log(sum(math.exp(x) for x in s))) < 1e-12
