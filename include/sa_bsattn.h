@@ -31,8 +31,10 @@
  * - stream: a hipStream_t passed as void* (NULL = the default stream).  All
  *   work is enqueued on it; no call synchronises unless its comment says so.
  *   Execution errors surface at the caller's next synchronisation.
- * - Supported shapes: d in {64, 128}; blk_q == blk_k in {64, 128}; B, H,
- *   N >= 1; n_kb <= 65535; B * H * n_qb < 2^31.  scale must be finite and > 0.
+ * - Supported shapes: d in {64, 128}; blk_q and blk_k each in {64, 128}
+ *   (the paper uses 128 x 128 blocks; a query block of 128 rows may also walk
+ *   64-key blocks and vice versa); B, H, N >= 1; n_kb <= 65535;
+ *   B * H * n_qb < 2^31.  scale must be finite and > 0.
  * - Every argument is validated before anything is enqueued: a non-zero
  *   return means nothing was launched and no output was written.
  */
@@ -71,6 +73,24 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v,
                          const uint64_t* mask_bits, void* out, float* lse,
                          int B, int H, int N, int d, int blk_q, int blk_k,
                          float scale, void* stream);
+
+/* Tensor layouts accepted by sa_bsattn_fwd_layout. */
+#define SA_LAYOUT_BHND 0 /* [B][H][N][d]: heads outermost (the other entry points) */
+#define SA_LAYOUT_BNHD 1 /* [B][N][H][d]: tokens outermost, as a DiT's projections emit */
+
+/*
+ * One-shot forward pass as sa_bsattn_fwd, with q, k, v and out in the layout
+ * named by `layout` (all four alike; lse stays float32 [B][H][N]).  In
+ * SA_LAYOUT_BNHD the rows of one head are H * d elements apart, so attention
+ * runs straight on the projection output without a transpose.  The result is
+ * bit-for-bit that of sa_bsattn_fwd on the transposed tensors.  Returns
+ * SA_ERR_INVALID_ARG for an unknown layout and SA_ERR_UNSUPPORTED when
+ * H * d * max(blk_q, blk_k) * 2 >= 2^31.
+ */
+SA_API int sa_bsattn_fwd_layout(const void* q, const void* k, const void* v,
+                                const uint64_t* mask_bits, void* out, float* lse, int B, int H,
+                                int N, int d, int blk_q, int blk_k, float scale, int layout,
+                                void* stream);
 
 /*
  * Mask pre-pass alone (the CRM walk of the paper's appendix "CRM Forward
@@ -132,7 +152,7 @@ SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
  * measured (the paper's appendix "Detailed Kernel Overhead Analysis" compares
  * its kernel at 0 % sparsity with a dense FlashAttention kernel).  The result
  * equals sa_bsattn_fwd with an all-ones mask bit for bit.  blk is the tile
- * size (64 or 128, as blk_q = blk_k above).  Arguments and errors otherwise as
+ * size (64 or 128, used for both query and key blocks).  Arguments and errors otherwise as
  * sa_bsattn_fwd.
  */
 SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,

@@ -16,6 +16,8 @@ SA_OK = 0
 SA_ERR_INVALID_ARG = 1
 SA_ERR_UNSUPPORTED = 2
 SA_ERR_HIP = 3
+SA_LAYOUT_BHND = 0
+SA_LAYOUT_BNHD = 1
 
 _LIB = None
 
@@ -37,6 +39,7 @@ SIGNATURES = {
     "sa_bsattn_plan_destroy": (_I, [_P]),
     "sa_dense_attn_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P]),
     "sa_mask_instantiate": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
+    "sa_bsattn_fwd_layout": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _P]),
     "sa_fidelity_profile": (_I, [_P, _P, _P, _I, _P, _P, _I, _P, _P, _P, _I, _I, _I, _I, _I, _F,
                                  _P]),
 }
@@ -140,6 +143,30 @@ def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
         _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
         B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
     _check("sa_bsattn_fwd", st)
+    return out, lse
+
+
+def bsattn_fwd_bnhd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
+                    stream=None):
+    """``sa_bsattn_fwd_layout`` with q, k, v, out in [B, N, H, d]; lse is [B, H, N]."""
+    torch = _torch()
+    lib = load()
+    B, N, H, d = q.shape
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    m = mask_to_device(mask_bits, q.device)
+    if m.dtype == torch.uint64:
+        m = m.view(torch.int64)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    st = lib.sa_bsattn_fwd_layout(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+        _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(m, torch.int64, "mask_bits"),
+        _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
+        B, H, N, d, int(blk_q), int(blk_k), float(scale), SA_LAYOUT_BNHD, _stream(stream))
+    _check("sa_bsattn_fwd_layout", st)
     return out, lse
 
 

@@ -33,7 +33,7 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Shape checks shared by every entry point that takes (B, H, N, blk_q, blk_k).
 int check_shape(int B, int H, int N, int blk_q, int blk_k, Dims* dims) {
   if (B < 1 || H < 1 || N < 1) return SA_ERR_INVALID_ARG;
-  if (blk_q != blk_k || (blk_q != 64 && blk_q != 128)) return SA_ERR_UNSUPPORTED;
+  if ((blk_q != 64 && blk_q != 128) || (blk_k != 64 && blk_k != 128)) return SA_ERR_UNSUPPORTED;
   const int n_qb = (N + blk_q - 1) / blk_q;
   const int n_kb = (N + blk_k - 1) / blk_k;
   if (n_kb > 65535) return SA_ERR_UNSUPPORTED;
@@ -155,19 +155,26 @@ SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
   if (st != SA_OK) return st;
   if (!counts || !lists || !order) return SA_ERR_INVALID_ARG;
   sa::AttnArgs a{q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k,
-                 dm.n_qb, dm.n_kb, scale};
+                 dm.n_qb, dm.n_kb, scale,
+                 (int64_t)H * N * d, (int64_t)N * d, d};
   return sa::launch_attention(a, (hipStream_t)stream) == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
-SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
-                         void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
-                         float scale, void* stream) {
+// One-shot forward for either tensor layout (strides in elements).
+static int fwd_oneshot(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
+                       void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
+                       float scale, int layout, void* stream) {
   Dims dm;
   int st = check_shape(B, H, N, blk_q, blk_k, &dm);
   if (st != SA_OK) return st;
   if (!mask_bits || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
+  if (layout != SA_LAYOUT_BHND && layout != SA_LAYOUT_BNHD) return SA_ERR_INVALID_ARG;
   st = check_tensors(q, k, v, mask_bits, H * dm.n_qb * dm.W, out, lse, B, H, N, d, scale);
   if (st != SA_OK) return st;
+  const bool bnhd = layout == SA_LAYOUT_BNHD;
+  const int sn = bnhd ? H * d : d;
+  // tile copies address a tile with 32-bit byte offsets
+  if ((int64_t)sn * (blk_k > blk_q ? blk_k : blk_q) * 2 >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
 
   hipStream_t s = (hipStream_t)stream;
   const Workspace w = plan_workspace(B, H, dm);
@@ -181,11 +188,26 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint
   if (e == hipSuccess) e = sa::launch_schedule(counts, B, H, dm.n_qb, order, s);
   if (e == hipSuccess) {
     sa::AttnArgs a{q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k,
-                   dm.n_qb, dm.n_kb, scale};
+                   dm.n_qb, dm.n_kb, scale,
+                   (int64_t)H * N * d, bnhd ? (int64_t)d : (int64_t)N * d, sn};
     e = sa::launch_attention(a, s);
   }
   const hipError_t ef = hipFreeAsync(ws, s);
   return (e == hipSuccess && ef == hipSuccess) ? SA_OK : SA_ERR_HIP;
+}
+
+SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
+                         void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
+                         float scale, void* stream) {
+  return fwd_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale,
+                     SA_LAYOUT_BHND, stream);
+}
+
+SA_API int sa_bsattn_fwd_layout(const void* q, const void* k, const void* v,
+                                const uint64_t* mask_bits, void* out, float* lse, int B, int H,
+                                int N, int d, int blk_q, int blk_k, float scale, int layout,
+                                void* stream) {
+  return fwd_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale, layout, stream);
 }
 
 SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
@@ -196,7 +218,8 @@ SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* 
   st = check_tensors(q, k, v, nullptr, 0, out, lse, B, H, N, d, scale);
   if (st != SA_OK) return st;
   sa::AttnArgs a{q, k, v, nullptr, nullptr, nullptr, out, lse, B, H, N, d, blk, blk,
-                 dm.n_qb, dm.n_kb, scale};
+                 dm.n_qb, dm.n_kb, scale,
+                 (int64_t)H * N * d, (int64_t)N * d, d};
   return sa::launch_attention_dense(a, (hipStream_t)stream) == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 

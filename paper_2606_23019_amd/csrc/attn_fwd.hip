@@ -102,43 +102,47 @@ __device__ __forceinline__ void copy16_to_lds(uint32_t lds_byte_addr, const void
                : "memory");
 }
 
-// Per-lane element offsets of a tile copy: lane l of load i writes the 16-byte
+// Per-lane byte offsets of a tile copy: lane l of load i writes the 16-byte
 // LDS chunk 64 (i + kLoadsPerWave * wave) + l, i.e. row r and physical chunk p;
-// the XOR swizzle is applied by reading source chunk p ^ swz(r).
+// the XOR swizzle is applied by reading source chunk p ^ swz(r).  Source rows
+// are sn elements apart (d for [B][H][N][d] tensors, H d for [B][N][H][d]).
 template <typename T, int D>
 struct CopyPlan {
-  uint32_t off[T::kLoadsPerWave];  // element offset inside a tile of D-wide rows
-  __device__ __forceinline__ void init(int wave, int lane) {
+  uint32_t off[T::kLoadsPerWave];  // byte offset inside the source tile
+  __device__ __forceinline__ void init(int wave, int lane, int sn) {
 #pragma unroll
     for (int i = 0; i < T::kLoadsPerWave; ++i) {
       const int idx = (wave * T::kLoadsPerWave + i) * 64 + lane;
       const int r = idx / T::kChunksPerRow;
       const int p = idx % T::kChunksPerRow;
-      off[i] = (uint32_t)(r * D + ((p ^ swz<D>(r)) << 3));
+      off[i] = (uint32_t)(r * sn + ((p ^ swz<D>(r)) << 3)) * 2u;
     }
   }
 };
 
-// Start copying rows key0 .. key0 + BK - 1 of a [N][D] bf16 matrix into an
+// Start copying rows key0 .. key0 + BK - 1 (rows sn elements apart) into an
 // LDS tile with global_load_lds_dwordx4 (no registers; completion is tracked
 // by vmcnt).  In a ragged last block, rows past N repeat row N - 1: finite
 // values whose logits are masked and whose probabilities are exactly zero.
 template <typename T, int BK, int D>
 __device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, int key0, int N,
-                                                int wave_u, const CopyPlan<T, D>& cp) {
-  const __bf16* tile = src + (int64_t)key0 * D;
+                                                int sn, int wave_u, int lane,
+                                                const CopyPlan<T, D>& cp) {
+  const __bf16* tile = src + (int64_t)key0 * sn;
   const uint32_t lds0 =
       (uint32_t)(uintptr_t)(SA_LDS void*)lds + (uint32_t)(wave_u * T::kLoadsPerWave * 1024);
   if (key0 + BK <= N) {
 #pragma unroll
-    for (int i = 0; i < T::kLoadsPerWave; ++i) copy16_to_lds(lds0 + i * 1024, tile, cp.off[i] * 2);
+    for (int i = 0; i < T::kLoadsPerWave; ++i) copy16_to_lds(lds0 + i * 1024, tile, cp.off[i]);
   } else {
-    const uint32_t last = (uint32_t)(N - 1 - key0) * D;  // first element of row N - 1
+    const int last = N - 1 - key0;  // last real row of this tile
 #pragma unroll
     for (int i = 0; i < T::kLoadsPerWave; ++i) {
-      const uint32_t rbase = cp.off[i] / D * D;
-      const uint32_t o = rbase <= last ? cp.off[i] : last + (cp.off[i] - rbase);
-      copy16_to_lds(lds0 + i * 1024, tile, o * 2);
+      const int idx = (wave_u * T::kLoadsPerWave + i) * 64 + lane;
+      const int r = idx / T::kChunksPerRow;
+      const int p = idx % T::kChunksPerRow;
+      const uint32_t o = (uint32_t)(min(r, last) * sn + ((p ^ swz<D>(r)) << 3)) * 2u;
+      copy16_to_lds(lds0 + i * 1024, tile, o);
     }
   }
 }
@@ -150,7 +154,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
-    int N, int n_qb, int n_kb, float c_log2) {
+    int N, int n_qb, int n_kb, float c_log2, int64_t sb, int64_t sh, int sn) {
   using T = Tile<BQ, BK, D>;
   constexpr int kL = T::kLoadsPerWave;
   __shared__ __attribute__((aligned(1024))) __bf16 Ks[BK * D];
@@ -171,18 +175,18 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   const int32_t* list = DENSE ? nullptr : lists + (int64_t)row * n_kb;
   // key block of the t-th enabled block (ascending, as the CRM walk yields them)
   auto kblk = [&](int t) { return DENSE ? t : list[t]; };
-  const int64_t base = (int64_t)bh * N * D;
+  const int64_t base = (int64_t)(bh / H) * sb + (int64_t)h * sh;  // element (b, h, token 0, 0)
   const __bf16* Qb = Q + base;
   const __bf16* Kb = K + base;
   const __bf16* Vb = V + base;
 
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   CopyPlan<T, D> cp;
-  cp.init(wave_u, lane);
+  cp.init(wave_u, lane, sn);
   if (cnt > 0) {
     const int key0 = kblk(0) * BK;
-    issue_tile_copy<T, BK, D>(Ks, Kb, key0, N, wave_u, cp);
-    issue_tile_copy<T, BK, D>(Vs, Vb, key0, N, wave_u, cp);
+    issue_tile_copy<T, BK, D>(Ks, Kb, key0, N, sn, wave_u, lane, cp);
+    issue_tile_copy<T, BK, D>(Vs, Vb, key0, N, sn, wave_u, lane, cp);
   }
 
   // Q^T fragments (B operand): lane holds Q[qrow][16 dc + 8 half .. +7].
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
 #pragma unroll
   for (int dc = 0; dc < D / 16; ++dc) {
     if (qrow < N)
-      qf[dc] = *(const bf16x8*)(Qb + (int64_t)qrow * D + dc * 16 + half * 8);
+      qf[dc] = *(const bf16x8*)(Qb + (int64_t)qrow * sn + dc * 16 + half * 8);
     else
       qf[dc] = bf16x8{};
   }
@@ -230,7 +234,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     }
 
     barrier_lds_reads_done();  // every wave is done with Ks
-    if (more) issue_tile_copy<T, BK, D>(Ks, Kb, key1, N, wave_u, cp);
+    if (more) issue_tile_copy<T, BK, D>(Ks, Kb, key1, N, sn, wave_u, lane, cp);
 
     if (key0 + BK > N) {  // ragged last block: keys >= N do not exist
 #pragma unroll
@@ -297,7 +301,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     }
 
     barrier_lds_reads_done();  // every wave is done with Vs
-    if (more) issue_tile_copy<T, BK, D>(Vs, Vb, key1, N, wave_u, cp);
+    if (more) issue_tile_copy<T, BK, D>(Vs, Vb, key1, N, sn, wave_u, lane, cp);
   }
 
   const float l_tot = l_run + other_half(l_run);
@@ -305,7 +309,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   if (qrow < N) {
     if (half == 0)
       LSE[(int64_t)bh * N + qrow] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
-    __bf16* orow = O + base + (int64_t)qrow * D;
+    __bf16* orow = O + base + (int64_t)qrow * sn;
 #pragma unroll
     for (int dg = 0; dg < D / 32; ++dg)
 #pragma unroll
@@ -323,19 +327,24 @@ hipError_t launch_tile(const AttnArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_items),
                      dim3(Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
                      (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
-                     (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e);
+                     (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
+                     a.sh, a.sn);
   return hipGetLastError();
+}
+
+template <int BQ, int BK, bool DENSE>
+hipError_t launch_d(const AttnArgs& a, hipStream_t stream) {
+  if (a.d == 128) return launch_tile<BQ, BK, 128, DENSE>(a, stream);
+  if (a.d == 64) return launch_tile<BQ, BK, 64, DENSE>(a, stream);
+  return hipErrorInvalidValue;
 }
 
 template <bool DENSE>
 hipError_t launch_any(const AttnArgs& a, hipStream_t stream) {
-  if (a.blk_q == 128 && a.blk_k == 128) {
-    if (a.d == 128) return launch_tile<128, 128, 128, DENSE>(a, stream);
-    if (a.d == 64) return launch_tile<128, 128, 64, DENSE>(a, stream);
-  } else if (a.blk_q == 64 && a.blk_k == 64) {
-    if (a.d == 128) return launch_tile<64, 64, 128, DENSE>(a, stream);
-    if (a.d == 64) return launch_tile<64, 64, 64, DENSE>(a, stream);
-  }
+  if (a.blk_q == 128 && a.blk_k == 128) return launch_d<128, 128, DENSE>(a, stream);
+  if (a.blk_q == 64 && a.blk_k == 64) return launch_d<64, 64, DENSE>(a, stream);
+  if (a.blk_q == 128 && a.blk_k == 64) return launch_d<128, 64, DENSE>(a, stream);
+  if (a.blk_q == 64 && a.blk_k == 128) return launch_d<64, 128, DENSE>(a, stream);
   return hipErrorInvalidValue;
 }
 

@@ -21,6 +21,9 @@ struct AttnArgs {
   float* lse;
   int B, H, N, d, blk_q, blk_k, n_qb, n_kb;
   float scale;
+  // element strides of q, k, v and out: batch, head, token (the head-dim is contiguous)
+  int64_t sb, sh;
+  int sn;
 };
 
 hipError_t launch_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,

@@ -66,7 +66,8 @@ def _fwd(lib, q=A, k=A + MB, v=A + 2 * MB, m=A + 3 * MB, out=A + 4 * MB, lse=A +
     (dict(scale=float("nan")), binding.SA_ERR_INVALID_ARG),
     (dict(scale=float("inf")), binding.SA_ERR_INVALID_ARG),
     (dict(d=96), binding.SA_ERR_UNSUPPORTED),
-    (dict(bq=64, bk=128), binding.SA_ERR_UNSUPPORTED),
+    (dict(bq=64, bk=32), binding.SA_ERR_UNSUPPORTED),
+    (dict(bq=256, bk=128), binding.SA_ERR_UNSUPPORTED),
     (dict(bq=32, bk=32), binding.SA_ERR_UNSUPPORTED),
     (dict(N=64 * 65536, bq=64, bk=64), binding.SA_ERR_UNSUPPORTED),  # n_kb > 65535
 ])
@@ -81,7 +82,7 @@ def test_other_entry_points_reject_bad_arguments(lib):
         binding.SA_ERR_UNSUPPORTED
     assert lib.sa_schedule(P(A), 0, 1, 1, P(A + MB), None) == binding.SA_ERR_INVALID_ARG
     h = P()
-    assert lib.sa_bsattn_plan_create(P(A), 1, 1, 100, 64, 128, None, ctypes.byref(h)) == \
+    assert lib.sa_bsattn_plan_create(P(A), 1, 1, 100, 64, 96, None, ctypes.byref(h)) == \
         binding.SA_ERR_UNSUPPORTED
     assert h.value is None
     assert lib.sa_bsattn_plan_create(P(A), 1, 1, 100, 64, 64, None, None) == \
@@ -170,3 +171,20 @@ def _fid(lib, q=A, k=A + MB, rows=A + 2 * MB, R=16, T=A + 3 * MB, p=A + 4 * MB, 
 ])
 def test_fidelity_rejects_bad_arguments_on_host(lib, kw, code):
     assert _fid(lib, **kw) == code
+
+
+def test_layout_entry_rejects_bad_arguments_on_host(lib):
+    P = ctypes.c_void_p
+
+    G = 1 << 34  # spacing wide enough that the large-H case does not overlap
+
+    def call(layout=1, H=2, d=128, q=A):
+        return lib.sa_bsattn_fwd_layout(P(q), P(A + G), P(A + 2 * G), P(A + 3 * G),
+                                        P(A + 4 * G), P(A + 5 * G), 1, H, 256, d, 128, 128,
+                                        ctypes.c_float(0.088), layout, None)
+    # every call carries at least one invalid argument
+    assert call(layout=2) == binding.SA_ERR_INVALID_ARG
+    assert call(layout=-1) == binding.SA_ERR_INVALID_ARG
+    assert call(q=0) == binding.SA_ERR_INVALID_ARG
+    assert call(d=96) == binding.SA_ERR_UNSUPPORTED
+    assert call(H=65536, d=128) == binding.SA_ERR_UNSUPPORTED   # row stride too large for a tile

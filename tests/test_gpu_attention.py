@@ -230,3 +230,87 @@ def test_invalid_arguments_write_nothing():
     assert (out == 7.0).all().item() and (lse == 7.0).all().item()
     with pytest.raises(binding.SAError):
         binding.bsattn_fwd(q, k, v, m, blk, blk, scale=-1.0)
+
+
+# ------------------------------------------------ query/key blocks of different size ---
+
+def _rect_mask(H, n_qb, n_kb, seed, p):
+    rng = np.random.default_rng(seed)
+    bm = rng.random((H, n_qb, n_kb)) < p
+    return bm
+
+
+MIXED = [
+    # (B, H, N, d, blk_q, blk_k, density, seed)
+    (1, 2, 1000, 128, 128, 64, 0.4, 71),   # ragged, 128-row query blocks on 64-key blocks
+    (2, 2, 1000, 64, 128, 64, 0.5, 72),
+    (1, 2, 1000, 128, 64, 128, 0.4, 73),   # 64-row query blocks on 128-key blocks
+    (2, 1, 777, 64, 64, 128, 0.6, 74),
+    (1, 1, 4096, 128, 128, 64, 1.0, 75),   # dense
+]
+
+
+@pytest.mark.parametrize("B,H,N,d,bq,bk,p,seed", MIXED)
+def test_parity_mixed_block_sizes(B, H, N, d, bq, bk, p, seed):
+    torch = _torch()
+    from paper_2606_23019_amd import binding
+    n_qb, n_kb = -(-N // bq), -(-N // bk)
+    bm = _rect_mask(H, n_qb, n_kb, seed, p)
+    bm[:, 0, :] = False                      # an empty row
+    packed = pack_rows(bm)
+    q, k, v = _rand_qkv(B, H, N, d, seed, scale=1.5)
+    out, lse = binding.bsattn_fwd(q, k, v, packed, bq, bk)
+    torch.cuda.synchronize()
+    ref_out, ref_lse = oracle.attention(to_bits(q), to_bits(k), to_bits(v), packed, bq, bk,
+                                        1.0 / d ** 0.5)
+    print(compare(out.float().cpu().numpy(), lse.cpu().numpy(), ref_out, ref_lse))
+    # the prepared and plan entry points agree bit for bit
+    counts, lists = binding.mask_prepass(packed, H, n_qb, n_kb)
+    order = binding.schedule(counts, B, H, n_qb)
+    o2, l2 = binding.bsattn_fwd_prepared(q, k, v, counts, lists, order, bq, bk)
+    plan = binding.Plan(packed, B, H, N, bq, bk)
+    o3, l3 = plan(q, k, v)
+    torch.cuda.synchronize()
+    assert torch.equal(o2, out) and torch.equal(l2, lse)
+    assert torch.equal(o3, out) and torch.equal(l3, lse)
+    plan.close()
+
+
+# ------------------------------------------------------------ [B, N, H, d] layout ---
+
+LAYOUT = [
+    # (B, H, N, d, blk_q, blk_k, density, seed)
+    (1, 3, 1000, 128, 128, 128, 0.4, 81),   # ragged
+    (2, 2, 777, 64, 64, 64, 0.5, 82),
+    (1, 4, 2048, 128, 128, 64, 0.3, 83),
+    (2, 1, 1000, 64, 64, 128, 1.0, 84),
+]
+
+
+@pytest.mark.parametrize("B,H,N,d,bq,bk,p,seed", LAYOUT)
+def test_bnhd_layout_matches_bhnd_bitwise(B, H, N, d, bq, bk, p, seed):
+    torch = _torch()
+    from paper_2606_23019_amd import binding
+    n_qb, n_kb = -(-N // bq), -(-N // bk)
+    packed = pack_rows(_rect_mask(H, n_qb, n_kb, seed, p))
+    q, k, v = _rand_qkv(B, H, N, d, seed)
+    o1, l1 = binding.bsattn_fwd(q, k, v, packed, bq, bk)
+    qt, kt, vt = (x.transpose(1, 2).contiguous() for x in (q, k, v))   # [B, N, H, d]
+    o2, l2 = binding.bsattn_fwd_bnhd(qt, kt, vt, packed, bq, bk)
+    torch.cuda.synchronize()
+    assert o2.shape == (B, N, H, d)
+    assert torch.equal(o2.transpose(1, 2), o1) and torch.equal(l2, l1)
+
+
+def test_bnhd_layout_parity_vs_reference():
+    torch = _torch()
+    from paper_2606_23019_amd import binding
+    B, H, N, d, blk = 2, 3, 1000, 128, 128
+    n = -(-N // blk)
+    packed = pack_rows(_rand_mask(H, n, 91, 0.5))
+    q, k, v = _rand_qkv(B, H, N, d, 91, scale=1.5)
+    out, lse = binding.bsattn_fwd_bnhd(*(x.transpose(1, 2).contiguous() for x in (q, k, v)),
+                                       packed, blk, blk)
+    torch.cuda.synchronize()
+    ref_out, ref_lse = _full_reference(q, k, v, packed, blk, 1.0 / d ** 0.5)
+    print(compare(out.transpose(1, 2).float().cpu().numpy(), lse.cpu().numpy(), ref_out, ref_lse))
