@@ -16,6 +16,8 @@ work), written to be checked against the paper by eye:
                    (Sec. 4.1.2) and CRM packing.
 * ``fidelity``   -- Hellinger distance and Fidelity Score (Sec. 4.2.1, Eq. 3-4)
                    of threshold-map masks on sampled rows (Sec. 4.2.3).
+* ``resize``     -- conservative bilinear-ceiling resize of masks and threshold
+                   maps between resolutions (Sec. 4.3.1, Eq. 7).
 * ``attention``  -- softmax attention restricted to the key blocks a query
                    block's CRM row enables (Sec. 4.3.2; mask instantiation
                    M_p = 1[T <= p] of Sec. 4.1.2 supplies the masks).
@@ -36,6 +38,7 @@ from .bits import (  # noqa: F401
 )
 from .masks import instantiate, instantiate_packed, pack_crm  # noqa: F401
 from .fidelity import hellinger, fidelity_score, profile  # noqa: F401
+from .resize import bilinear_ceil, resize_mask, resize_threshold_map  # noqa: F401
 from .attention import (  # noqa: F401
     attention_block,
     attention,
