@@ -376,6 +376,44 @@ def run_fidelity(path, steps, warmup):
     return rows_out
 
 
+def run_resize(path, steps, warmup):
+    """Threshold-map and mask resize 480p -> 720p (40 heads, 256^2 -> 591^2 blocks) and a
+    4x upscale of 720p maps, against HBM: each base entry read (cached re-reads are
+    not counted), each target entry written."""
+    import torch
+    from paper_2606_23019_amd import binding
+    from workloads import SHORT
+    a, b = SHORT["14b-480p"], SHORT["14b-720p"]
+    rows = []
+    for label, H, nq, tq in (("480p->720p", a.H, a.n_qb, b.n_qb), ("720p->4x", b.H, b.n_qb, 4 * b.n_qb)):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(6000 + tq)
+        T = torch.rand((H, nq, nq), generator=g, device="cuda")
+        masks = binding.mask_instantiate(T, torch.full((1, H), 0.3, device="cuda"))[0].contiguous()
+        for kind in ("map", "mask"):
+            if kind == "map":
+                def fn():
+                    binding.resize_threshold_map(T, tq, tq)
+                nbytes = 4.0 * H * nq * nq + 4.0 * H * tq * tq
+            else:
+                def fn():
+                    binding.resize_mask(masks, nq, tq, tq)
+                nbytes = 8.0 * H * nq * ((nq + 63) // 64) + 8.0 * H * tq * ((tq + 63) // 64)
+            for _ in range(warmup):
+                fn()
+            t, _ = _per_launch_time(fn, steps)
+            rec = dict(resize=label, kind=kind, H=H, base=nq, target=tq, us=t * 1e3,
+                       algorithmic_bytes=nbytes, gbs=nbytes / (t * 1e-3) / 1e9,
+                       frac_hbm_peak=nbytes / (t * 1e-3) / 1e9 / PEAK_HBM_GBS)
+            log(json.dumps(rec))
+            rows.append(rec)
+        del T, masks
+        torch.cuda.empty_cache()
+    with open(path, "w") as f:
+        json.dump(rows, f, indent=1)
+    return rows
+
+
 COPY_BYTES = 1 << 30
 
 
@@ -411,6 +449,8 @@ def main():
                     help="also time mask instantiation from threshold maps into this file")
     ap.add_argument("--fidelity", default=None,
                     help="also time the Hellinger fidelity profile into this file")
+    ap.add_argument("--resize", default=None,
+                    help="also time the conservative resize of maps and masks into this file")
     ap.add_argument("--profile", action="store_true",
                     help="counter-collection run: attention kernel launches plus a plain 1 GiB "
                          "device copy (the HBM byte-counter calibration), nothing else")
@@ -528,6 +568,8 @@ def main():
         run_instantiate(args.instantiate, args.steps, args.warmup)
     if args.fidelity:
         run_fidelity(args.fidelity, args.steps, args.warmup)
+    if args.resize:
+        run_resize(args.resize, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(rec), flush=True)

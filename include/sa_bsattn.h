@@ -123,6 +123,35 @@ SA_API int sa_mask_instantiate(const float* T, const float* p, int n_p, int H, i
                                uint64_t* mask_bits, void* stream);
 
 /*
+ * Conservative resize between resolutions (Sec. 4.3.1, Eq. 7): masks and
+ * maps are built once at a base resolution and resized for others.  Target
+ * block (u, v) samples the base at x = u * n_qb / n_qb_out,
+ * y = v * n_kb / n_kb_out (exact rationals); its bilinear neighbours with a
+ * positive weight are base rows floor(x) and, if x is not whole,
+ * floor(x) + 1 (the last row repeats past the end), likewise for columns.
+ *
+ * sa_resize_mask: CRM bits [H][n_qb][W] -> [H][n_qb_out][W_out]; a target
+ * bit is the ceiling of the bilinear interpolation of the 0/1 mask, i.e. the
+ * OR of its positively weighted neighbours.  Every output word is written
+ * (bits past n_kb_out zero).
+ *
+ * sa_resize_threshold_map: float32 [H][n_qb][n_kb] -> [H][n_qb_out][n_kb_out];
+ * a target entry is the minimum of its positively weighted neighbours (NaN
+ * entries skipped), the reading of Eq. 7 for threshold maps under which
+ * sa_mask_instantiate(resized map, p) == sa_resize_mask(sa_mask_instantiate
+ * (map, p)) for every p.
+ *
+ * Meant for upscaling (every active base block survives); a smaller target
+ * samples only some base rows.  Outputs must not overlap inputs.  All sizes
+ * (H included) >= 1 and <= 65535.
+ */
+SA_API int sa_resize_mask(const uint64_t* mask_bits, int H, int n_qb, int n_kb, uint64_t* mask_out,
+                          int n_qb_out, int n_kb_out, void* stream);
+
+SA_API int sa_resize_threshold_map(const float* T, int H, int n_qb, int n_kb, float* T_out,
+                                   int n_qb_out, int n_kb_out, void* stream);
+
+/*
  * Work schedule (balances heads of uneven density): writes order[0 .. B*H*n_qb-1],
  * a permutation of the work items it = (b * H + h) * n_qb + u.  Items of one
  * (b, h) stay together in ascending u; (b, h) groups are ordered by

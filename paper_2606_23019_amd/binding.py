@@ -40,6 +40,8 @@ SIGNATURES = {
     "sa_dense_attn_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P]),
     "sa_mask_instantiate": (_I, [_P, _P, _I, _I, _I, _I, _P, _P]),
     "sa_bsattn_fwd_layout": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _P]),
+    "sa_resize_mask": (_I, [_P, _I, _I, _I, _P, _I, _I, _P]),
+    "sa_resize_threshold_map": (_I, [_P, _I, _I, _I, _P, _I, _I, _P]),
     "sa_fidelity_profile": (_I, [_P, _P, _P, _I, _P, _P, _I, _P, _P, _P, _I, _I, _I, _I, _I, _F,
                                  _P]),
 }
@@ -236,6 +238,35 @@ def fidelity_profile(q, k, rows, T, p, blk, scale=None, stream=None):
         B, H, N, d, int(blk), float(scale), _stream(stream))
     _check("sa_fidelity_profile", st)
     return hel, fid, blk_lse
+
+
+def resize_threshold_map(T, n_qb_out, n_kb_out, stream=None):
+    """``sa_resize_threshold_map``: float32 [H, n_qb, n_kb] -> [H, n_qb_out, n_kb_out]."""
+    torch = _torch()
+    lib = load()
+    H, n_qb, n_kb = T.shape
+    out = torch.empty((H, n_qb_out, n_kb_out), dtype=torch.float32, device=T.device)
+    st = lib.sa_resize_threshold_map(_dev_ptr(T, torch.float32, "T"), H, n_qb, n_kb,
+                                     _dev_ptr(out, torch.float32, "T_out"), n_qb_out, n_kb_out,
+                                     _stream(stream))
+    _check("sa_resize_threshold_map", st)
+    return out
+
+
+def resize_mask(mask_bits, n_kb, n_qb_out, n_kb_out, stream=None):
+    """``sa_resize_mask``: CRM int64 [H, n_qb, W] (n_kb key blocks) -> [H, n_qb_out, W_out]."""
+    torch = _torch()
+    lib = load()
+    m = mask_to_device(mask_bits)
+    if m.dtype == torch.uint64:
+        m = m.view(torch.int64)
+    H, n_qb, _ = m.shape
+    out = torch.full((H, n_qb_out, (n_kb_out + 63) // 64), -1, dtype=torch.int64, device=m.device)
+    st = lib.sa_resize_mask(_dev_ptr(m, torch.int64, "mask_bits"), H, n_qb, n_kb,
+                            _dev_ptr(out, torch.int64, "mask_out"), n_qb_out, n_kb_out,
+                            _stream(stream))
+    _check("sa_resize_mask", st)
+    return out
 
 
 def mask_prepass(mask_bits, H, n_qb, n_kb, stream=None):

@@ -17,7 +17,7 @@ LIB_NAME = "libsa_bsattn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "prepass.hip", "mask_inst.hip", "fidelity.hip", "attn_fwd.hip"]
+SOURCES = ["api.cpp", "prepass.hip", "mask_inst.hip", "fidelity.hip", "resize.hip", "attn_fwd.hip"]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=" + ARCH,

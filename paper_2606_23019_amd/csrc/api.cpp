@@ -136,6 +136,40 @@ SA_API int sa_mask_instantiate(const float* T, const float* p, int n_p, int H, i
   return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
+static int check_resize(const void* in, size_t in_align, int H, int nq, int nk, const void* out,
+                        size_t out_align, int tq, int tk) {
+  if (!in || !out || H < 1 || nq < 1 || nk < 1 || tq < 1 || tk < 1) return SA_ERR_INVALID_ARG;
+  if (!aligned(in, in_align) || !aligned(out, out_align)) return SA_ERR_INVALID_ARG;
+  if (nq > 65535 || nk > 65535 || tq > 65535 || tk > 65535 || H > 65535) return SA_ERR_UNSUPPORTED;
+  if ((int64_t)H * tq * tk >= ((int64_t)1 << 40) || (int64_t)H * nq >= ((int64_t)1 << 31) ||
+      (int64_t)H * tq >= ((int64_t)1 << 31))
+    return SA_ERR_UNSUPPORTED;
+  return SA_OK;
+}
+
+SA_API int sa_resize_threshold_map(const float* T, int H, int n_qb, int n_kb, float* T_out,
+                                   int n_qb_out, int n_kb_out, void* stream) {
+  int st = check_resize(T, 4, H, n_qb, n_kb, T_out, 4, n_qb_out, n_kb_out);
+  if (st != SA_OK) return st;
+  if (overlap(T_out, (size_t)H * n_qb_out * n_kb_out * 4, T, (size_t)H * n_qb * n_kb * 4))
+    return SA_ERR_INVALID_ARG;
+  const hipError_t e =
+      sa::launch_resize_map(T, H, n_qb, n_kb, T_out, n_qb_out, n_kb_out, (hipStream_t)stream);
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
+SA_API int sa_resize_mask(const uint64_t* mask_bits, int H, int n_qb, int n_kb, uint64_t* mask_out,
+                          int n_qb_out, int n_kb_out, void* stream) {
+  int st = check_resize(mask_bits, 8, H, n_qb, n_kb, mask_out, 8, n_qb_out, n_kb_out);
+  if (st != SA_OK) return st;
+  const size_t in_bytes = (size_t)H * n_qb * ((n_kb + 63) / 64) * 8;
+  const size_t out_bytes = (size_t)H * n_qb_out * ((n_kb_out + 63) / 64) * 8;
+  if (overlap(mask_out, out_bytes, mask_bits, in_bytes)) return SA_ERR_INVALID_ARG;
+  const hipError_t e = sa::launch_resize_mask(mask_bits, H, n_qb, n_kb, mask_out, n_qb_out,
+                                              n_kb_out, (hipStream_t)stream);
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
+}
+
 SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* order, void* stream) {
   if (!counts || !order || B < 1 || H < 1 || n_qb < 1) return SA_ERR_INVALID_ARG;
   if (!aligned(counts, 4) || !aligned(order, 4)) return SA_ERR_INVALID_ARG;

@@ -35,6 +35,12 @@ hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_
 hipError_t launch_mask_instantiate(const float* T, const float* p, int n_p, int H, int n_qb,
                                    int n_kb, uint64_t* bits, hipStream_t stream);
 
+hipError_t launch_resize_map(const float* T, int H, int nq, int nk, float* out, int tq, int tk,
+                             hipStream_t stream);
+
+hipError_t launch_resize_mask(const uint64_t* bits, int H, int nq, int nk, uint64_t* out, int tq,
+                              int tk, hipStream_t stream);
+
 bool fidelity_supported(int R, int K);
 
 hipError_t launch_fidelity(const void* q, const void* k, const int32_t* rows, int R, const float* T,

@@ -188,3 +188,18 @@ def test_layout_entry_rejects_bad_arguments_on_host(lib):
     assert call(q=0) == binding.SA_ERR_INVALID_ARG
     assert call(d=96) == binding.SA_ERR_UNSUPPORTED
     assert call(H=65536, d=128) == binding.SA_ERR_UNSUPPORTED   # row stride too large for a tile
+
+
+@pytest.mark.parametrize("fn", ["sa_resize_mask", "sa_resize_threshold_map"])
+def test_resize_rejects_bad_arguments_on_host(lib, fn):
+    P = ctypes.c_void_p
+    f = getattr(lib, fn)
+    # every call carries at least one invalid argument
+    assert f(None, 1, 4, 4, P(A + MB), 8, 8, None) == binding.SA_ERR_INVALID_ARG
+    assert f(P(A), 1, 4, 4, None, 8, 8, None) == binding.SA_ERR_INVALID_ARG
+    assert f(P(A + 2), 1, 4, 4, P(A + MB), 8, 8, None) == binding.SA_ERR_INVALID_ARG
+    assert f(P(A), 0, 4, 4, P(A + MB), 8, 8, None) == binding.SA_ERR_INVALID_ARG
+    assert f(P(A), 1, 4, 4, P(A + MB), 0, 8, None) == binding.SA_ERR_INVALID_ARG
+    assert f(P(A), 1, 4, 4, P(A + 8), 8, 8, None) == binding.SA_ERR_INVALID_ARG   # overlap
+    assert f(P(A), 1, 4, 70000, P(A + MB), 8, 8, None) == binding.SA_ERR_UNSUPPORTED
+    assert f(P(A), 1, 4, 4, P(A + MB), 8, 70000, None) == binding.SA_ERR_UNSUPPORTED
