@@ -147,6 +147,31 @@ __device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, 
   }
 }
 
+// Loads i0 .. i0 + count - 1 of a tile copy (count and i0 are compile-time
+// constants wherever this is inlined into an unrolled loop).
+template <typename T, int BK, int D>
+__device__ __forceinline__ void issue_tile_slice(__bf16* lds, const __bf16* src, int key0, int N,
+                                                 int sn, int wave_u, int lane,
+                                                 const CopyPlan<T, D>& cp, int i0, int count) {
+  const __bf16* tile = src + (int64_t)key0 * sn;
+  const uint32_t lds0 =
+      (uint32_t)(uintptr_t)(SA_LDS void*)lds + (uint32_t)(wave_u * T::kLoadsPerWave * 1024);
+  if (key0 + BK <= N) {
+#pragma unroll
+    for (int i = i0; i < i0 + count; ++i) copy16_to_lds(lds0 + i * 1024, tile, cp.off[i]);
+  } else {
+    const int last = N - 1 - key0;
+#pragma unroll
+    for (int i = i0; i < i0 + count; ++i) {
+      const int idx = (wave_u * T::kLoadsPerWave + i) * 64 + lane;
+      const int r = idx / T::kChunksPerRow;
+      const int p = idx % T::kChunksPerRow;
+      const uint32_t o = (uint32_t)(min(r, last) * sn + ((p ^ swz<D>(r)) << 3)) * 2u;
+      copy16_to_lds(lds0 + i * 1024, tile, o);
+    }
+  }
+}
+
 // DENSE = true is the maskless path: item i is processed by workgroup i and
 // every key block 0 .. n_kb - 1 is enabled (counts, lists and order unused).
 template <int BQ, int BK, int D, bool DENSE>
@@ -183,11 +208,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   CopyPlan<T, D> cp;
   cp.init(wave_u, lane, sn);
-  if (cnt > 0) {
-    const int key0 = kblk(0) * BK;
-    issue_tile_copy<T, BK, D>(Ks, Kb, key0, N, sn, wave_u, lane, cp);
-    issue_tile_copy<T, BK, D>(Vs, Vb, key0, N, sn, wave_u, lane, cp);
-  }
+  if (cnt > 0) issue_tile_copy<T, BK, D>(Ks, Kb, kblk(0) * BK, N, sn, wave_u, lane, cp);
 
   // Q^T fragments (B operand): lane holds Q[qrow][16 dc + 8 half .. +7].
   const int qrow = u * BQ + wave * 32 + l32;
@@ -213,12 +234,19 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   const int g = lane >> 4;
   const int j = lane & 15;
 
+  // Copies are issued in slices between compute steps rather than in one
+  // burst per tile: V[t] in BK / 32 slices between the key groups of S[t]
+  // (its buffer is free once P V[t-1] is done), K[t+1] in two halves inside
+  // the softmax of block t (its buffer is free once S[t] is done).  Bursts of
+  // copies queue behind each other at issue and hold up the wavefront.
+  constexpr int kVSlice = kL / (BK / 32);
+  static_assert(kL % (BK / 32) == 0 && kL % 2 == 0, "copy slices");
   for (int t = 0; t < cnt; ++t) {
     const int key0 = kblk(t) * BK;
     const bool more = t + 1 < cnt;
     const int key1 = more ? kblk(t + 1) * BK : 0;
 
-    barrier_copies_landed<kL>();  // K[t] landed (V[t] may still be in flight)
+    barrier_copies_landed<0>();  // K[t] landed (no younger copy is in flight)
 
     // S^T = K Q^T, one 32-key group per accumulator.
     f32x16 s[BK / 32];
@@ -231,10 +259,10 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
         const bf16x8 a = lds_read_b128(Ks + kr * D + (((2 * dc + half) ^ swz<D>(kr)) << 3));
         s[kg] = mfma32x32x16(a, qf[dc], s[kg]);
       }
+      issue_tile_slice<T, BK, D>(Vs, Vb, key0, N, sn, wave_u, lane, cp, kg * kVSlice, kVSlice);
     }
 
     barrier_lds_reads_done();  // every wave is done with Ks
-    if (more) issue_tile_copy<T, BK, D>(Ks, Kb, key1, N, sn, wave_u, lane, cp);
 
     if (key0 + BK > N) {  // ragged last block: keys >= N do not exist
 #pragma unroll
@@ -252,6 +280,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kg][i]);
     mx = fmaxf(mx, other_half(mx)) * c_log2;
+    if (more) issue_tile_slice<T, BK, D>(Ks, Kb, key1, N, sn, wave_u, lane, cp, 0, kL / 2);
     // Rescale only when some row's maximum grew.  Keeping the exact running
     // maximum (rather than a stale one) makes each row's largest probability
     // exactly 1, which bf16 represents without error.
@@ -268,7 +297,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     bf16x8 pf[BK / 16];
     float lsum = 0.f;
 #pragma unroll
-    for (int kg = 0; kg < BK / 32; ++kg)
+    for (int kg = 0; kg < BK / 32; ++kg) {
 #pragma unroll
       for (int j8 = 0; j8 < 2; ++j8)
 #pragma unroll
@@ -277,6 +306,9 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
           lsum += p;
           pf[2 * kg + j8][e] = (__bf16)p;
         }
+      if (kg == (BK / 32 - 1) / 2 && more)
+        issue_tile_slice<T, BK, D>(Ks, Kb, key1, N, sn, wave_u, lane, cp, kL / 2, kL / 2);
+    }
     l_run += lsum;
 
     if (more)
@@ -301,22 +333,28 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
     }
 
     barrier_lds_reads_done();  // every wave is done with Vs
-    if (more) issue_tile_copy<T, BK, D>(Vs, Vb, key1, N, sn, wave_u, lane, cp);
   }
 
+  // Epilogue addresses are rebuilt from the wave-uniform row base and a lane
+  // id recomputed here (mbcnt), so that nothing formed before the loop has to
+  // stay live across it.
   const float l_tot = l_run + other_half(l_run);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-  if (qrow < N) {
-    if (half == 0)
-      LSE[(int64_t)bh * N + qrow] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
-    __bf16* orow = O + base + (int64_t)qrow * sn;
+  const int lane_e = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int l32_e = lane_e & 31;
+  const int half_e = lane_e >> 5;
+  const int row0 = u * BQ + wave_u * 32;  // first query row of this wavefront
+  if (row0 + l32_e < N) {
+    if (half_e == 0)
+      LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
+    __bf16* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
 #pragma unroll
     for (int dg = 0; dg < D / 32; ++dg)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const bf16x4 w = {(__bf16)(o[dg][4 * r4 + 0] * inv), (__bf16)(o[dg][4 * r4 + 1] * inv),
                           (__bf16)(o[dg][4 * r4 + 2] * inv), (__bf16)(o[dg][4 * r4 + 3] * inv)};
-        *(bf16x4*)(orow + dg * 32 + 8 * r4 + 4 * half) = w;
+        *(bf16x4*)(orow + dg * 32 + 8 * r4 + 4 * half_e) = w;
       }
   }
 }
