@@ -66,9 +66,9 @@ def reference_items(q, k, v, packed, blk_q, blk_k, scale, items):
     for (b, h), us in sorted(by_head.items()):
         kb = to_bits(k[b, h])
         vb = to_bits(v[b, h])
-        allowed = oracle.block_mask(packed[h:h + 1], n_kb)[0]
         for u in us:
+            allowed = oracle.block_mask(packed[h:h + 1, u:u + 1], n_kb)[0, 0]
             r0, r1 = u * blk_q, min((u + 1) * blk_q, N)
             qb = to_bits(q[b, h, r0:r1])
-            res[(b, h, u)] = oracle.attention_block(qb, kb, vb, allowed[u], blk_k, scale)
+            res[(b, h, u)] = oracle.attention_block(qb, kb, vb, allowed, blk_k, scale)
     return res

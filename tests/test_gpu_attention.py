@@ -314,3 +314,40 @@ def test_bnhd_layout_parity_vs_reference():
     torch.cuda.synchronize()
     ref_out, ref_lse = _full_reference(q, k, v, packed, blk, 1.0 / d ** 0.5)
     print(compare(out.transpose(1, 2).float().cpu().numpy(), lse.cpu().numpy(), ref_out, ref_lse))
+
+
+# ------------------------------------------------------------------- maximum size ---
+
+def test_largest_supported_row_n_kb_65535():
+    # 65535 key blocks of 64 (N = 4 194 240 tokens, the ABI's row limit), one head,
+    # d = 64; each query row enables the diagonal, the first and the last block
+    # and two seeded random blocks.  Sampled query blocks vs the reference.
+    torch = _torch()
+    from paper_2606_23019_amd import binding
+    B, H, d, blk = 1, 1, 64, 64
+    n = 65535
+    N = n * blk
+    W = -(-n // 64)
+    rng = np.random.default_rng(123)
+    packed = np.zeros((H, n, W), dtype=np.uint64)
+    u = np.arange(n)
+    cols = np.stack([u, np.zeros(n, int), np.full(n, n - 1), rng.integers(0, n, n),
+                     rng.integers(0, n, n)], axis=1)
+    for c in range(cols.shape[1]):
+        v = cols[:, c]
+        np.bitwise_or.at(packed[0], (u, v // 64), np.uint64(1) << (v % 64).astype(np.uint64))
+    q, k, v_ = _rand_qkv(B, H, N, d, 124)
+    out, lse = binding.bsattn_fwd(q, k, v_, packed, blk, blk)
+    torch.cuda.synchronize()
+    items = [(0, 0, x) for x in (0, 1, 777, 32768, n - 2, n - 1)]
+    ref = reference_items(q, k, v_, packed, blk, blk, d ** -0.5, items)
+    go, gl, ro, rl = [], [], [], []
+    for (b, h, uu) in items:
+        go.append(out[b, h, uu * blk:(uu + 1) * blk].float().cpu().numpy())
+        gl.append(lse[b, h, uu * blk:(uu + 1) * blk].cpu().numpy())
+        ro.append(ref[(b, h, uu)][0])
+        rl.append(ref[(b, h, uu)][1])
+    print(compare(np.concatenate(go), np.concatenate(gl), np.concatenate(ro), np.concatenate(rl)))
+    assert torch.isfinite(lse).all().item()
+    del q, k, v_, out, lse
+    torch.cuda.empty_cache()
