@@ -224,7 +224,11 @@ typedef struct sa_plan* sa_plan_t;
 SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
                                  int blk_q, int blk_k, void* stream, sa_plan_t* plan);
 
-/* Attention with a plan: only the attention kernel is enqueued. */
+/*
+ * Attention with a plan: only the attention kernel is enqueued (no
+ * allocation, memset or synchronisation), so the call may be captured into a
+ * HIP graph and replayed; the plan and the tensors must outlive the graph.
+ */
 SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v,
                               void* out, float* lse, int d, float scale, void* stream);
 
