@@ -166,7 +166,11 @@ SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb,
  * Attention kernel alone, on a pre-computed pre-pass and schedule (the
  * static-mask case: masks are built once and reused for every prompt,
  * Sec. 4 overview figure, "Reuse for All Prompts").  counts/lists/order as produced
- * by sa_mask_prepass and sa_schedule for the same (B, H, N, blk_q, blk_k).
+ * by sa_mask_prepass and sa_schedule for the same (B, H, N, blk_q, blk_k),
+ * 4-byte aligned.  Entries out of range are clamped on the device (work item
+ * to [0, B H n_qb), count to [0, n_kb], key block to [0, n_kb)): the result
+ * of malformed buffers is unspecified, but nothing outside the tensors is
+ * read or written.
  */
 SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
                                   const int32_t* counts, const int32_t* lists,
@@ -225,7 +229,8 @@ SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
                                  int blk_q, int blk_k, void* stream, sa_plan_t* plan);
 
 /*
- * Attention with a plan: only the attention kernel is enqueued (no
+ * Attention with a plan (on the device that was current at creation, else
+ * SA_ERR_INVALID_ARG): only the attention kernel is enqueued (no
  * allocation, memset or synchronisation), so the call may be captured into a
  * HIP graph and replayed; the plan and the tensors must outlive the graph.
  */

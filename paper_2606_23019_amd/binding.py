@@ -105,6 +105,35 @@ def _dev_ptr(t, dtype, name):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _need(cond, msg):
+    """Size checks on the host: the C ABI takes raw pointers and cannot see buffer sizes."""
+    if not cond:
+        raise ValueError(msg)
+
+
+def _same_shape(ref, others, names):
+    for t, n in zip(others, names):
+        _need(tuple(t.shape) == tuple(ref.shape), "%s has shape %s, expected %s"
+              % (n, tuple(t.shape), tuple(ref.shape)))
+
+
+def _outputs(q, out, lse, lse_shape):
+    torch = _torch()
+    if out is None:
+        out = torch.empty_like(q)
+    _need(tuple(out.shape) == tuple(q.shape), "out must have the shape of q")
+    if lse is None:
+        lse = torch.empty(lse_shape, dtype=torch.float32, device=q.device)
+    _need(tuple(lse.shape) == tuple(lse_shape), "lse must have shape %s" % (tuple(lse_shape),))
+    return out, lse
+
+
+def _mask_words(m, H, n_qb, n_kb):
+    _need(m.numel() == H * n_qb * ((n_kb + 63) // 64),
+          "mask has %d words, expected H * n_qb * ceil(n_kb / 64) = %d"
+          % (m.numel(), H * n_qb * ((n_kb + 63) // 64)))
+
+
 def _stream(stream):
     torch = _torch()
     if stream is None:
@@ -130,15 +159,14 @@ def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
     torch = _torch()
     lib = load()
     B, H, N, d = q.shape
+    _same_shape(q, (k, v), ("k", "v"))
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
     m = mask_to_device(mask_bits, q.device)
     if m.dtype == torch.uint64:
         m = m.view(torch.int64)
-    if out is None:
-        out = torch.empty_like(q)
-    if lse is None:
-        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    _mask_words(m, H, -(-N // int(blk_q)), -(-N // int(blk_k)))
+    out, lse = _outputs(q, out, lse, (B, H, N))
     st = lib.sa_bsattn_fwd(
         _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
         _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(m, torch.int64, "mask_bits"),
@@ -154,15 +182,14 @@ def bsattn_fwd_bnhd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=
     torch = _torch()
     lib = load()
     B, N, H, d = q.shape
+    _same_shape(q, (k, v), ("k", "v"))
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
     m = mask_to_device(mask_bits, q.device)
     if m.dtype == torch.uint64:
         m = m.view(torch.int64)
-    if out is None:
-        out = torch.empty_like(q)
-    if lse is None:
-        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    _mask_words(m, H, -(-N // int(blk_q)), -(-N // int(blk_k)))
+    out, lse = _outputs(q, out, lse, (B, H, N))
     st = lib.sa_bsattn_fwd_layout(
         _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
         _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(m, torch.int64, "mask_bits"),
@@ -177,12 +204,10 @@ def dense_attn_fwd(q, k, v, blk=128, scale=None, out=None, lse=None, stream=None
     torch = _torch()
     lib = load()
     B, H, N, d = q.shape
+    _same_shape(q, (k, v), ("k", "v"))
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
-    if out is None:
-        out = torch.empty_like(q)
-    if lse is None:
-        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    out, lse = _outputs(q, out, lse, (B, H, N))
     st = lib.sa_dense_attn_fwd(
         _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
         _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, torch.bfloat16, "out"),
@@ -206,6 +231,7 @@ def mask_instantiate(T, p, out=None, stream=None):
     W = (n_kb + 63) // 64
     if out is None:
         out = torch.empty((n_p, H, n_qb, W), dtype=torch.int64, device=T.device)
+    _need(out.numel() == n_p * H * n_qb * W, "out must hold n_p * H * n_qb * W words")
     st = lib.sa_mask_instantiate(_dev_ptr(T, torch.float32, "T"), _dev_ptr(p, torch.float32, "p"),
                                  n_p, H, n_qb, n_kb, _dev_ptr(out, torch.int64, "mask_bits"),
                                  _stream(stream))
@@ -221,9 +247,13 @@ def fidelity_profile(q, k, rows, T, p, blk, scale=None, stream=None):
     torch = _torch()
     lib = load()
     B, H, N, d = q.shape
+    _same_shape(q, (k,), ("k",))
+    _need(rows.dim() == 2 and rows.shape[0] == H, "rows must be [H, R]")
     R = rows.shape[1]
+    _need(p.dim() == 1, "p must be [K]")
     K = p.shape[0]
     n_kb = (N + blk - 1) // blk
+    _need(tuple(T.shape) == (H, n_kb, n_kb), "T must be [H, n_qb, n_kb] = %s" % ((H, n_kb, n_kb),))
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
     dev = q.device
@@ -261,6 +291,7 @@ def resize_mask(mask_bits, n_kb, n_qb_out, n_kb_out, stream=None):
     if m.dtype == torch.uint64:
         m = m.view(torch.int64)
     H, n_qb, _ = m.shape
+    _mask_words(m, H, n_qb, n_kb)
     out = torch.full((H, n_qb_out, (n_kb_out + 63) // 64), -1, dtype=torch.int64, device=m.device)
     st = lib.sa_resize_mask(_dev_ptr(m, torch.int64, "mask_bits"), H, n_qb, n_kb,
                             _dev_ptr(out, torch.int64, "mask_out"), n_qb_out, n_kb_out,
@@ -273,7 +304,10 @@ def mask_prepass(mask_bits, H, n_qb, n_kb, stream=None):
     """``sa_mask_prepass``: returns (counts int32 [H*n_qb], lists int32 [H*n_qb, n_kb])."""
     torch = _torch()
     lib = load()
-    m = mask_to_device(mask_bits)
+    m = mask_to_device(mask_bits, mask_bits.device if isinstance(mask_bits, torch.Tensor) else "cuda")
+    if m.dtype == torch.uint64:
+        m = m.view(torch.int64)
+    _mask_words(m, H, n_qb, n_kb)
     counts = torch.full((H * n_qb,), -1, dtype=torch.int32, device=m.device)
     lists = torch.full((H * n_qb, n_kb), -1, dtype=torch.int32, device=m.device)
     st = lib.sa_mask_prepass(_dev_ptr(m, torch.int64, "mask_bits"), H, n_qb, n_kb,
@@ -287,6 +321,7 @@ def schedule(counts, B, H, n_qb, stream=None):
     """``sa_schedule``: returns order int32 [B*H*n_qb]."""
     torch = _torch()
     lib = load()
+    _need(counts.numel() == H * n_qb, "counts must hold H * n_qb entries")
     order = torch.full((B * H * n_qb,), -1, dtype=torch.int32, device=counts.device)
     st = lib.sa_schedule(_dev_ptr(counts, torch.int32, "counts"), B, H, n_qb,
                          _dev_ptr(order, torch.int32, "order"), _stream(stream))
@@ -300,12 +335,14 @@ def bsattn_fwd_prepared(q, k, v, counts, lists, order, blk_q, blk_k, scale=None,
     torch = _torch()
     lib = load()
     B, H, N, d = q.shape
+    _same_shape(q, (k, v), ("k", "v"))
+    n_qb, n_kb = -(-N // int(blk_q)), -(-N // int(blk_k))
+    _need(counts.numel() == H * n_qb, "counts must hold H * n_qb entries")
+    _need(lists.numel() == H * n_qb * n_kb, "lists must hold H * n_qb * n_kb entries")
+    _need(order.numel() == B * H * n_qb, "order must hold B * H * n_qb entries")
     if scale is None:
         scale = 1.0 / float(d) ** 0.5
-    if out is None:
-        out = torch.empty_like(q)
-    if lse is None:
-        lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+    out, lse = _outputs(q, out, lse, (B, H, N))
     st = lib.sa_bsattn_fwd_prepared(
         _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
         _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(counts, torch.int32, "counts"),
@@ -323,6 +360,9 @@ class Plan:
         torch = _torch()
         self._lib = load()
         self._m = mask_to_device(mask_bits)
+        if self._m.dtype == torch.uint64:
+            self._m = self._m.view(torch.int64)
+        _mask_words(self._m, H, -(-N // int(blk_q)), -(-N // int(blk_k)))
         self.B, self.H, self.N, self.blk_q, self.blk_k = B, H, N, blk_q, blk_k
         h = ctypes.c_void_p()
         st = self._lib.sa_bsattn_plan_create(_dev_ptr(self._m, torch.int64, "mask_bits"), B, H, N,
@@ -341,12 +381,10 @@ class Plan:
         B, H, N, d = q.shape
         if (B, H, N) != (self.B, self.H, self.N):
             raise ValueError("q shape %s does not match the plan" % (tuple(q.shape),))
+        _same_shape(q, (k, v), ("k", "v"))
         if scale is None:
             scale = 1.0 / float(d) ** 0.5
-        if out is None:
-            out = torch.empty_like(q)
-        if lse is None:
-            lse = torch.empty((B, H, N), dtype=torch.float32, device=q.device)
+        out, lse = _outputs(q, out, lse, (B, H, N))
         st = self._lib.sa_bsattn_fwd_plan(
             self._h, _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
             _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, torch.bfloat16, "out"),

@@ -34,8 +34,8 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 int check_shape(int B, int H, int N, int blk_q, int blk_k, Dims* dims) {
   if (B < 1 || H < 1 || N < 1) return SA_ERR_INVALID_ARG;
   if ((blk_q != 64 && blk_q != 128) || (blk_k != 64 && blk_k != 128)) return SA_ERR_UNSUPPORTED;
-  const int n_qb = (N + blk_q - 1) / blk_q;
-  const int n_kb = (N + blk_k - 1) / blk_k;
+  const int n_qb = (int)(((int64_t)N + blk_q - 1) / blk_q);
+  const int n_kb = (int)(((int64_t)N + blk_k - 1) / blk_k);
   if (n_kb > 65535) return SA_ERR_UNSUPPORTED;
   if ((int64_t)B * H * n_qb >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
   dims->n_qb = n_qb;
@@ -44,7 +44,7 @@ int check_shape(int B, int H, int N, int blk_q, int blk_k, Dims* dims) {
   return SA_OK;
 }
 
-int check_tensors(const void* q, const void* k, const void* v, const void* mask_bits, int mask_words,
+int check_tensors(const void* q, const void* k, const void* v, const void* mask_bits, size_t mask_words,
                   const void* out, const float* lse, int B, int H, int N, int d, float scale) {
   if (d != 64 && d != 128) return SA_ERR_UNSUPPORTED;
   if (!(scale > 0.f) || !isfinite(scale)) return SA_ERR_INVALID_ARG;
@@ -188,6 +188,7 @@ SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
   st = check_tensors(q, k, v, nullptr, 0, out, lse, B, H, N, d, scale);
   if (st != SA_OK) return st;
   if (!counts || !lists || !order) return SA_ERR_INVALID_ARG;
+  if (!aligned(counts, 4) || !aligned(lists, 4) || !aligned(order, 4)) return SA_ERR_INVALID_ARG;
   sa::AttnArgs a{q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k,
                  dm.n_qb, dm.n_kb, scale,
                  (int64_t)H * N * d, (int64_t)N * d, d};
@@ -203,7 +204,7 @@ static int fwd_oneshot(const void* q, const void* k, const void* v, const uint64
   if (st != SA_OK) return st;
   if (!mask_bits || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
   if (layout != SA_LAYOUT_BHND && layout != SA_LAYOUT_BNHD) return SA_ERR_INVALID_ARG;
-  st = check_tensors(q, k, v, mask_bits, H * dm.n_qb * dm.W, out, lse, B, H, N, d, scale);
+  st = check_tensors(q, k, v, mask_bits, (size_t)H * dm.n_qb * dm.W, out, lse, B, H, N, d, scale);
   if (st != SA_OK) return st;
   const bool bnhd = layout == SA_LAYOUT_BNHD;
   const int sn = bnhd ? H * d : d;
@@ -340,6 +341,9 @@ SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
 SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v,
                               void* out, float* lse, int d, float scale, void* stream) {
   if (!plan) return SA_ERR_INVALID_ARG;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SA_ERR_HIP;
+  if (dev != plan->device) return SA_ERR_INVALID_ARG;  // the plan's buffers live on its device
   return sa_bsattn_fwd_prepared(q, k, v, plan->counts, plan->lists, plan->order, out, lse, plan->B,
                                 plan->H, plan->N, d, plan->blk_q, plan->blk_k, scale, stream);
 }

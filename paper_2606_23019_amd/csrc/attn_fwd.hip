@@ -191,15 +191,19 @@ __global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
   const int half = lane >> 5;
   const int l32 = lane & 31;
 
-  const int item = DENSE ? (int)blockIdx.x : order[blockIdx.x];
+  // Work item, row count and key blocks come from caller-visible buffers
+  // (sa_bsattn_fwd_prepared): they are clamped into range, so malformed
+  // input gives wrong values but never an access outside the tensors.
+  const int n_items = (int)gridDim.x;
+  const int item = DENSE ? (int)blockIdx.x : min(max(order[blockIdx.x], 0), n_items - 1);
   const int bh = item / n_qb;
   const int u = item - bh * n_qb;
   const int h = bh % H;
   const int row = h * n_qb + u;
-  const int cnt = DENSE ? n_kb : counts[row];
+  const int cnt = DENSE ? n_kb : min(max(counts[row], 0), n_kb);
   const int32_t* list = DENSE ? nullptr : lists + (int64_t)row * n_kb;
   // key block of the t-th enabled block (ascending, as the CRM walk yields them)
-  auto kblk = [&](int t) { return DENSE ? t : list[t]; };
+  auto kblk = [&](int t) { return DENSE ? t : min(max(list[t], 0), n_kb - 1); };
   const int64_t base = (int64_t)(bh / H) * sb + (int64_t)h * sh;  // element (b, h, token 0, 0)
   const __bf16* Qb = Q + base;
   const __bf16* Kb = K + base;

@@ -2,6 +2,8 @@
 arguments on the host before touching the GPU (no compute calls here)."""
 
 import ctypes
+
+import numpy as np
 import os
 import re
 
@@ -203,3 +205,32 @@ def test_resize_rejects_bad_arguments_on_host(lib, fn):
     assert f(P(A), 1, 4, 4, P(A + 8), 8, 8, None) == binding.SA_ERR_INVALID_ARG   # overlap
     assert f(P(A), 1, 4, 70000, P(A + MB), 8, 8, None) == binding.SA_ERR_UNSUPPORTED
     assert f(P(A), 1, 4, 4, P(A + MB), 8, 70000, None) == binding.SA_ERR_UNSUPPORTED
+
+
+# ------------------------------------------- binding size checks (host only) ---
+
+def test_binding_rejects_mismatched_sizes_before_any_device_call():
+    import torch
+    from paper_2606_23019_amd import binding
+    q = torch.zeros((1, 2, 256, 64), dtype=torch.bfloat16)
+    good_mask = np.zeros((2, 2, 1), dtype=np.uint64)          # H=2, n_qb=2 (blk 128), W=1
+    with pytest.raises(ValueError):
+        binding.bsattn_fwd(q, q, q, np.zeros((2, 1, 1), dtype=np.uint64), 128, 128)  # short mask
+    with pytest.raises(ValueError):
+        binding.bsattn_fwd(q, q[:, :1], q, good_mask, 128, 128)                      # k shape
+    with pytest.raises(ValueError):
+        binding.bsattn_fwd(q, q, q, good_mask, 128, 128,
+                           lse=torch.zeros((1, 2, 255)))                              # lse shape
+    with pytest.raises(ValueError):
+        binding.bsattn_fwd_bnhd(q, q, q, np.zeros((256, 2, 1), dtype=np.uint64), 128, 128)
+    with pytest.raises(ValueError):
+        binding.dense_attn_fwd(q, q, q[..., :32])
+    with pytest.raises(ValueError):
+        binding.mask_prepass(torch.zeros((2, 2, 2), dtype=torch.int64), 2, 2, 2)     # 2 words for 1
+    with pytest.raises(ValueError):
+        binding.bsattn_fwd_prepared(q, q, q, torch.zeros(4, dtype=torch.int32),
+                                    torch.zeros(7, dtype=torch.int32),
+                                    torch.zeros(4, dtype=torch.int32), 128, 128)
+    with pytest.raises(ValueError):
+        binding.fidelity_profile(q, q, torch.zeros((2, 4), dtype=torch.int32),
+                                 torch.zeros((2, 3, 2)), torch.zeros(3), 128)         # T shape

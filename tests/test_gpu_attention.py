@@ -351,3 +351,24 @@ def test_largest_supported_row_n_kb_65535():
     assert torch.isfinite(lse).all().item()
     del q, k, v_, out, lse
     torch.cuda.empty_cache()
+
+
+def test_malformed_prepared_buffers_are_clamped():
+    # counts past n_kb or negative, key blocks and work items out of range: the
+    # kernel clamps them into range (unspecified values, no access outside)
+    torch = _torch()
+    from paper_2606_23019_amd import binding
+    B, H, N, d, blk = 1, 2, 1000, 128, 128
+    n = -(-N // blk)
+    q, k, v = _rand_qkv(B, H, N, d, 95)
+    counts = torch.tensor([n + 5, -2, 3, 0, n, 1, 2, 7] * 2, dtype=torch.int32, device="cuda")
+    lists = torch.randint(-5, 10 ** 6, (H * n, n), dtype=torch.int32, device="cuda")
+    order = torch.tensor([-1, 10 ** 9] + list(range(B * H * n - 2)), dtype=torch.int32,
+                         device="cuda")
+    # duplicated work items leave others unprocessed: start from zeros so that
+    # every row is finite whether or not a workgroup wrote it
+    out = torch.zeros_like(q)
+    lse = torch.zeros((B, H, N), dtype=torch.float32, device="cuda")
+    binding.bsattn_fwd_prepared(q, k, v, counts, lists, order, blk, blk, out=out, lse=lse)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all().item()
