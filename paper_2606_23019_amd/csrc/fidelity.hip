@@ -17,9 +17,9 @@
 // straight from global memory as the A operand.  Each lane then holds one
 // row's logits for its half of the keys; the block's log-sum-exp is a lane
 // reduction plus one exchange between the half-wavefronts.
-// Kernel 2 (one wavefront per sampled row): the row's dense log-normaliser
-// from its block log-masses, then for each candidate p the dropped mass over
-// blocks with !(T <= p) and H from the closed form above.  Kernel 3 averages
+// Kernel 2 (one wavefront per sampled row, one lane per candidate): the row's
+// dense log-normaliser from its block log-masses, then for each candidate p
+// the dropped mass over blocks with !(T <= p) and H from the closed form above.  Kernel 3 averages
 // 1 - H over a head's rows into the Fidelity Score (Eq. 4).
 
 #include <math.h>
@@ -59,21 +59,35 @@ __global__ __launch_bounds__(64 * kFidWaves) void fid_block_mass_kernel(
                        : bf16x8{};
   }
 
-  const int v_first = blockIdx.x * (kFidWaves * kFidBlocksPerWave);
-  for (int t = 0; t < kFidBlocksPerWave; ++t) {
-    const int v = v_first + t * kFidWaves + wave;
-    if (v >= n_kb) break;  // uniform per wavefront
-    const int key_lo = v * blk;
-    const int key_hi = min(key_lo + blk, N);
-    float mx = -INFINITY;
-    float sum = 0.f;  // sum of exp2(s - mx) over this lane's keys
-    for (int g0 = key_lo; g0 < key_hi; g0 += 32) {
-      const int key = min(g0 + l32, N - 1);
-      const __bf16* krow = K + base + (int64_t)key * D;
-      bf16x8 kf[D / 16];
+  // This wavefront's key blocks are v_first + t * kFidWaves + wave; they are
+  // walked as one stream of 32-key groups, and the next group's K fragments
+  // are requested before the current group's MFMAs so that loads overlap.
+  const int v_first = blockIdx.x * (kFidWaves * kFidBlocksPerWave) + wave;
+  int n_blocks = 0;  // blocks of this wavefront that exist
+  while (n_blocks < kFidBlocksPerWave && v_first + n_blocks * kFidWaves < n_kb) ++n_blocks;
+  if (n_blocks == 0) return;  // uniform per wavefront; no workgroup barrier below
+  const int gpb = blk / 32;   // 32-key groups per block
+
+  auto group_key0 = [&](int j) { return (v_first + (j / gpb) * kFidWaves) * blk + (j % gpb) * 32; };
+  auto load_group = [&](int j, bf16x8 (&kf)[D / 16]) {
+    const int key = min(group_key0(j) + l32, N - 1);
+    const __bf16* krow = K + base + (int64_t)key * D;
 #pragma unroll
-      for (int dc = 0; dc < D / 16; ++dc) kf[dc] = *(const bf16x8*)(krow + dc * 16 + half * 8);
-      f32x16 s = {};
+    for (int dc = 0; dc < D / 16; ++dc) kf[dc] = *(const bf16x8*)(krow + dc * 16 + half * 8);
+  };
+
+  const int n_groups = n_blocks * gpb;
+  bf16x8 kf[D / 16], kn[D / 16];
+  load_group(0, kf);
+  float mx = -INFINITY;
+  float sum = 0.f;  // sum of exp2(s - mx) over this lane's keys of the current block
+  for (int j = 0; j < n_groups; ++j) {
+    if (j + 1 < n_groups) load_group(j + 1, kn);
+    const int v = v_first + (j / gpb) * kFidWaves;
+    const int key_hi = min((v + 1) * blk, N);
+    const int g0 = group_key0(j);
+    f32x16 s = {};
+    if (g0 < key_hi) {  // uniform; groups wholly past N hold no key
 #pragma unroll
       for (int dc = 0; dc < D / 16; ++dc) s = mfma32x32x16(kf[dc], qf[dc], s);
       // register i: key g0 + 8 (i / 4) + 4 half + i % 4 of this lane's row
@@ -93,14 +107,19 @@ __global__ __launch_bounds__(64 * kFidWaves) void fid_block_mass_kernel(
         mx = nmx;
       }
     }
-    // combine the two half-wavefronts (same row, different keys)
-    const float omx = other_half(mx);
-    const float osum = other_half(sum);
-    const float tmx = fmaxf(mx, omx);
-    const float tsum = (mx == -INFINITY ? 0.f : sum * fast_exp2(mx - tmx)) +
-                       (omx == -INFINITY ? 0.f : osum * fast_exp2(omx - tmx));
-    if (half == 0 && l32 < R)
-      blk_lse[((int64_t)bh * R + l32) * n_kb + v] = (tmx + fast_log2(tsum)) * kLn2F;
+    if (j % gpb == gpb - 1) {  // last group of block v: combine the half-wavefronts
+      const float omx = other_half(mx);
+      const float osum = other_half(sum);
+      const float tmx = fmaxf(mx, omx);
+      const float tsum = (mx == -INFINITY ? 0.f : sum * fast_exp2(mx - tmx)) +
+                         (omx == -INFINITY ? 0.f : osum * fast_exp2(omx - tmx));
+      if (half == 0 && l32 < R)
+        blk_lse[((int64_t)bh * R + l32) * n_kb + v] = (tmx + fast_log2(tsum)) * kLn2F;
+      mx = -INFINITY;
+      sum = 0.f;
+    }
+#pragma unroll
+    for (int dc = 0; dc < D / 16; ++dc) kf[dc] = kn[dc];
   }
 }
 
@@ -118,7 +137,12 @@ __device__ __forceinline__ float wave_sum(float x) {
 constexpr int kFidMaxR = 32;
 constexpr int kFidMaxK = 64;
 
-// One wavefront per sampled row (b, h, i).
+// One wavefront per sampled row (b, h, i); lane c owns candidate c (K <= 64).
+// The row's dense log-normaliser comes from its block log-masses (lanes over
+// blocks), then every lane walks all blocks: the block's mass and map entry
+// are the same for the whole wavefront, and lane c adds the mass when the
+// block is off for its threshold.  Each block costs a few instructions
+// whatever the number of candidates, and no per-candidate reduction is left.
 __global__ __launch_bounds__(64 * kFidWaves) void fid_row_kernel(
     const float* __restrict__ blk_lse, const int32_t* __restrict__ rows, int R,
     const float* __restrict__ T, const float* __restrict__ p, int K, int H, int N, int blk,
@@ -137,22 +161,21 @@ __global__ __launch_bounds__(64 * kFidWaves) void fid_row_kernel(
   float z = 0.f;
   for (int v = lane; v < n_kb; v += 64) z += __expf(lrow[v] - mx);
   const float lse = mx + __logf(wave_sum(z));
-  for (int c = 0; c < K; ++c) {
-    const float pc = p[c];
-    float dropped = 0.f;
-    int kept = 0;
-    for (int v = lane; v < n_kb; v += 64) {
-      if (trow[v] <= pc)  // NaN on either side: block off
-        ++kept;
-      else
-        dropped += __expf(lrow[v] - lse);
-    }
-    dropped = fminf(fmaxf(wave_sum(dropped), 0.f), 1.f);
-    const int any_kept = __any(kept > 0);
-    if (lane == 0)
-      hel[((int64_t)bh * R + i) * K + c] =
-          any_kept ? sqrtf(dropped / (1.f + sqrtf(1.f - dropped))) : 1.f;
+  const float pc = lane < K ? p[lane] : 0.f;
+  float dropped = 0.f;
+  bool kept = false;
+#pragma unroll 8
+  for (int v = 0; v < n_kb; ++v) {
+    const float t = trow[v];                 // wavefront-uniform address
+    const float mass = __expf(lrow[v] - lse);
+    if (t <= pc)                             // NaN on either side: block off
+      kept = true;
+    else
+      dropped += mass;
   }
+  dropped = fminf(fmaxf(dropped, 0.f), 1.f);
+  if (lane < K)
+    hel[((int64_t)bh * R + i) * K + lane] = kept ? sqrtf(dropped / (1.f + sqrtf(1.f - dropped))) : 1.f;
 }
 
 // Fidelity Score per (b, h, candidate): 1 - mean over the sampled rows.
