@@ -174,8 +174,14 @@ __device__ __forceinline__ void issue_tile_slice(__bf16* lds, const __bf16* src,
 
 // DENSE = true is the maskless path: item i is processed by workgroup i and
 // every key block 0 .. n_kb - 1 is enabled (counts, lists and order unused).
+// Occupancy hint (waves per SIMD): two, except for 64 x 128 tiles with d = 128
+// (two wavefronts own 128 keys of S and P each), which need more than 256
+// registers per wave and run one.
+template <int BQ, int BK, int D>
+constexpr int kWavesPerSimd = (BQ == 64 && BK == 128 && D == 128) ? 1 : 2;
+
 template <int BQ, int BK, int D, bool DENSE>
-__global__ __launch_bounds__(BQ / 32 * 64, 2) void bsattn_fwd_kernel(
+__global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsattn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
