@@ -56,6 +56,8 @@ SMALL = [
     (1, 1, 130, 128, 128, 1.0, 7),     # last block holds 2 keys
     (1, 2, 2048, 128, 128, 0.3, 8),
     (1, 1, 64, 64, 64, 1.0, 9),        # a single block
+    (1, 1, 1, 64, 64, 1.0, 10),        # one token: a single ragged block of one key
+    (3, 2, 5, 128, 128, 1.0, 11),      # N below one block, B > 1
 ]
 
 
@@ -94,6 +96,27 @@ def test_edge_rows_empty_first_last_only():
     ref_out, ref_lse = _full_reference(q, k, v, packed, blk, 1.0 / d ** 0.5)
     print(compare(out, lse, ref_out, ref_lse))
     assert np.all(out[0, 0, 3 * blk:(n - 1) * blk] == 0.0)
+
+
+def test_all_empty_mask_writes_zeros_and_neg_inf():
+    """No enabled block anywhere: every output row is 0 and every lse is -inf,
+    through the one-shot call and through a plan."""
+    from paper_2606_23019_amd import binding
+    torch = _torch()
+    B, H, N, d, blk = 2, 3, 700, 128, 128
+    n = -(-N // blk)
+    packed = pack_rows(np.zeros((H, n, n), dtype=bool))
+    q, k, v = _rand_qkv(B, H, N, d, 41)
+    out, lse = _run(q, k, v, packed, blk)
+    assert np.all(out == 0.0) and np.all(np.isneginf(lse))
+    plan = binding.Plan(packed, B, H, N, blk, blk)
+    out2 = torch.full_like(q, 7.0)
+    lse2 = torch.zeros((B, H, N), dtype=torch.float32, device="cuda")
+    assert plan.executed_blocks == 0
+    plan(q, k, v, 1.0 / d ** 0.5, out=out2, lse=lse2)
+    torch.cuda.synchronize()
+    plan.close()
+    assert (out2 == 0).all().item() and torch.isneginf(lse2).all().item()
 
 
 def test_large_logits_stay_finite():
