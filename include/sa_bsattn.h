@@ -152,12 +152,17 @@ SA_API int sa_resize_threshold_map(const float* T, int H, int n_qb, int n_kb, fl
                                    int n_qb_out, int n_kb_out, void* stream);
 
 /*
- * Work schedule (balances heads of uneven density): writes order[0 .. B*H*n_qb-1],
- * a permutation of the work items it = (b * H + h) * n_qb + u.  Items of one
- * (b, h) stay together in ascending u; (b, h) groups are ordered by
- * decreasing total enabled blocks (largest first, ties by index) so that the
- * heaviest heads start first.  counts: device int32 [H * n_qb] from the
- * pre-pass.  order: device int32 [B * H * n_qb].
+ * Work schedule (balances heads of uneven density and keeps K/V reuse inside
+ * each XCD's L2): writes order[0 .. B*H*n_qb-1], a permutation of the work
+ * items it = (b * H + h) * n_qb + u; the attention kernel runs item order[p]
+ * at launch position p, and position p runs on XCD p mod 8.  The (b, h)
+ * groups are ranked by decreasing total enabled blocks (ties by index).
+ * With q = n_qb / 8 and r = n_qb mod 8, the group of rank k is cut into 8
+ * chunks of consecutive u, chunk x holding q items plus one more when x is one
+ * of (k r + i) mod 8, i < r.  Positions x, x + 8, x + 16, ... hold chunk x of
+ * every group in rank order, each chunk in ascending u.  counts: device int32
+ * [H * n_qb] from the pre-pass.  order: device int32 [B * H * n_qb].  With
+ * more than 4096 (b, h) groups the order is the identity.
  */
 SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb,
                        int32_t* order, void* stream);

@@ -10,11 +10,19 @@
 // The attention kernel then reads a dense list instead of decoding bits.
 //
 // Schedule: heads have very different densities, so (b, h) groups are
-// started heaviest first.  One workgroup computes each head's total enabled
-// blocks, sorts the groups with a bitonic network in LDS, and writes the item
-// order; items inside a group stay in ascending query-block order so that
-// neighbouring query blocks, which share most key blocks in structured
-// masks, run close together in time.
+// started heaviest first, and the order is laid out for the 8 XCDs, each
+// with its own L2.  Workgroups are dealt to the XCDs round-robin (launch
+// position p runs on XCD p mod 8, in increasing p), so the order is written
+// as 8 interleaved sequences: sequence x holds chunk x of every group, the
+// groups heaviest first, where a group's n_qb query blocks are cut into 8
+// consecutive chunks of n_qb / 8 (the n_qb mod 8 leftover items rotate over
+// the XCDs from group to group, which makes every sequence exactly as long
+// as the positions p = x mod 8).  Each XCD thus works on a few groups at a
+// time, on neighbouring query blocks that share most key blocks in
+// structured masks, so their K/V tiles are reused from its L2, and every XCD
+// gets an equal slice of every group, so the load stays balanced.  One
+// workgroup computes each group's total enabled blocks, sorts the groups
+// with a bitonic network in LDS and writes the order.
 
 #include "device_common.h"
 #include "launch.h"
@@ -61,6 +69,7 @@ __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
 }
 
 constexpr int kSchedThreads = 1024;
+constexpr int kXcds = 8;  // accelerator complex dies of an MI355X, one L2 each
 
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ counts,
                                                                   int B, int H, int n_qb,
@@ -105,11 +114,29 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
       __syncthreads();
     }
   }
-  for (int64_t i = tid; i < n_items; i += kSchedThreads) {
-    const int p = (int)(i / n_qb);
-    const int u = (int)(i - (int64_t)p * n_qb);
-    const int unit = (int)(keys[p] & 0xFFFFFFFFu);
-    order[i] = unit * n_qb + u;
+  // Position pos = x + 8 j is item j of sequence x.  Group of rank k gives
+  // sequence x the chunk of s(k, x) = q + e(k, x) items, e(k, x) = 1 for the
+  // r sequences (k r + i) mod 8, i < r.  prefix(k) counts the items of the
+  // ranks before k in sequence x: k q plus the t < k r with t = x (mod 8).
+  const int q = n_qb / kXcds;
+  const int r = n_qb - q * kXcds;
+  for (int64_t pos = tid; pos < n_items; pos += kSchedThreads) {
+    const int x = (int)(pos % kXcds);
+    const int64_t j = pos / kXcds;
+    auto prefix = [&](int k) -> int64_t {
+      const int64_t t = (int64_t)k * r - x;
+      return (int64_t)k * q + (t > 0 ? (t + kXcds - 1) / kXcds : 0);
+    };
+    // average chunk n_qb / 8 gives the rank to within a few steps
+    const int64_t k_est = j * kXcds / n_qb;
+    int k = (int)(k_est < n_units - 1 ? k_est : n_units - 1);
+    while (k + 1 < n_units && prefix(k + 1) <= j) ++k;
+    while (k > 0 && prefix(k) > j) --k;
+    int before = 0;  // sequences x' < x that take one of this group's leftover items
+    for (int i = 0; i < r; ++i) before += ((k * r + i) % kXcds) < x;
+    const int u = x * q + before + (int)(j - prefix(k));
+    const int unit = (int)(keys[k] & 0xFFFFFFFFu);
+    order[pos] = unit * n_qb + u;
   }
 }
 

@@ -76,10 +76,32 @@ def test_prepass_ignores_bits_past_last_block():
         assert np.array_equal(a[r, :n[r]], b[r, :n[r]])
 
 
-def test_schedule_is_a_heaviest_first_permutation():
+def _xcd_order(units_sorted, n_qb, xcds=8):
+    """The documented order, built literally: sequence x gets chunk x of every
+    group (groups heaviest first), chunks of n_qb // 8 items plus one leftover
+    item for the sequences (k r + i) mod 8, i < r = n_qb mod 8, of the group of
+    rank k; position x + 8 j holds item j of sequence x."""
+    q, r = divmod(n_qb, xcds)
+    seqs = [[] for _ in range(xcds)]
+    for k, unit in enumerate(units_sorted):
+        extra = {(k * r + i) % xcds for i in range(r)}
+        start = 0
+        for x in range(xcds):
+            size = q + (1 if x in extra else 0)
+            seqs[x].extend(unit * n_qb + u for u in range(start, start + size))
+            start += size
+    order = [None] * (len(units_sorted) * n_qb)
+    for x, seq in enumerate(seqs):
+        for j, item in enumerate(seq):
+            order[x + xcds * j] = item
+    return order
+
+
+@pytest.mark.parametrize("n", [48, 45, 3, 256])
+def test_schedule_is_an_xcd_sliced_heaviest_first_permutation(n):
     from paper_2606_23019_amd import binding
-    rng = np.random.default_rng(11)
-    H, n = 7, 48
+    rng = np.random.default_rng(11 + n)
+    H = 7
     dens = rng.uniform(0.02, 0.9, size=H)
     dens[3] = dens[5]                              # a tie between two heads
     bm = np.stack([rng.random((n, n)) < p for p in dens])
@@ -90,11 +112,17 @@ def test_schedule_is_a_heaviest_first_permutation():
         order = binding.schedule(counts, B, H, n).cpu().numpy()
         assert sorted(order.tolist()) == list(range(B * H * n))
         cost = bm.reshape(H, -1).sum(axis=1)
-        groups = order.reshape(B * H, n)
-        units = groups[:, 0] // n
-        for g, unit in zip(groups, units):
-            assert g.tolist() == [unit * n + u for u in range(n)]
-        unit_cost = [cost[unit % H] for unit in units]
-        expect = sorted(range(B * H), key=lambda x: (-cost[x % H], x))
-        assert units.tolist() == expect
-        assert all(a >= b for a, b in zip(unit_cost, unit_cost[1:]))
+        units = sorted(range(B * H), key=lambda x: (-cost[x % H], x))
+        assert order.tolist() == _xcd_order(units, n)
+        # every XCD slot (positions = x mod 8) visits the groups heaviest first,
+        # each group's items in one ascending run of consecutive query blocks
+        for x in range(8):
+            seq = order[x::8]
+            groups = seq // n
+            runs = [g for i, g in enumerate(groups) if i == 0 or g != groups[i - 1]]
+            assert len(runs) == len(set(runs))
+            c = [cost[g % H] for g in runs]
+            assert all(a >= b for a, b in zip(c, c[1:]))
+            for g in set(runs):
+                us = seq[groups == g] % n
+                assert np.all(np.diff(us) == 1)
