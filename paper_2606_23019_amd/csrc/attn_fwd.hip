@@ -172,8 +172,9 @@ __device__ __forceinline__ void issue_tile_slice(__bf16* lds, const __bf16* src,
   }
 }
 
-// DENSE = true is the maskless path: item i is processed by workgroup i and
-// every key block 0 .. n_kb - 1 is enabled (counts, lists and order unused).
+// DENSE = true is the maskless path: every key block 0 .. n_kb - 1 is enabled
+// (counts, lists and order unused) and the items are laid out for the XCDs
+// as the schedule lays them out, with the (b, h) groups in index order.
 // Occupancy hint (waves per SIMD): two, except for 64 x 128 tiles with d = 128
 // (two wavefronts own 128 keys of S and P each), which need more than 256
 // registers per wave and run one.
@@ -201,7 +202,14 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
   // (sa_bsattn_fwd_prepared): they are clamped into range, so malformed
   // input gives wrong values but never an access outside the tensors.
   const int n_items = (int)gridDim.x;
-  const int item = DENSE ? (int)blockIdx.x : min(max(order[blockIdx.x], 0), n_items - 1);
+  int item;
+  if (DENSE) {  // every group costs the same: the XCD layout of the schedule, groups in index order
+    int uu;
+    const int unit = xcd_slice(blockIdx.x, n_items / n_qb, n_qb, &uu);
+    item = min(max(unit * n_qb + uu, 0), n_items - 1);
+  } else {
+    item = min(max(order[blockIdx.x], 0), n_items - 1);
+  }
   const int bh = item / n_qb;
   const int u = item - bh * n_qb;
   const int h = bh % H;

@@ -43,6 +43,43 @@ __device__ __forceinline__ void lds_write_b128(__bf16* p, u32x4 v) {
 // Value held by lane l ^ 32.
 __device__ __forceinline__ float other_half(float x) { return __shfl_xor(x, 32, 64); }
 
+// Work layout for the XCDs.  Launch position pos runs on XCD pos mod 8 (the
+// dispatcher deals workgroups round-robin), and each XCD takes its positions
+// in increasing order.  Given n_units groups of n_qb items, ranked 0 ..
+// n_units - 1, position pos = x + 8 j is item j of sequence x, where sequence
+// x holds chunk x of every group in rank order: a group's items are cut into 8
+// runs of consecutive u, run x holding q = n_qb / 8 items plus one when x is
+// one of (k r + i) mod 8, i < r = n_qb mod 8, for the group of rank k (the
+// leftovers rotate, so every sequence is exactly as long as its share of
+// positions).  Returns the rank k and writes the item's u.
+constexpr int kXcds = 8;  // accelerator complex dies of an MI355X, one L2 each
+
+__device__ __forceinline__ int xcd_slice(int64_t pos, int n_units, int n_qb, int* u_out) {
+  const int q = n_qb / kXcds;
+  const int r = n_qb - q * kXcds;
+  const int x = (int)(pos % kXcds);
+  const int64_t j = pos / kXcds;
+  // items of sequence x in the groups of rank < k: k q plus the t < k r with t = x (mod 8)
+  auto prefix = [&](int k) -> int64_t {
+    const int64_t t = (int64_t)k * r - x;
+    return (int64_t)k * q + (t > 0 ? (t + kXcds - 1) / kXcds : 0);
+  };
+  // k0 = floor(8 j / n_qb) has prefix(k0) <= j (k0 q + ceil(k0 r / 8) <= j
+  // since 8 k0 q + k0 r <= 8 j), and the rank is at most 1 + 7 / n_qb above
+  // it, so a fixed number of forward steps finds it; the steps and the
+  // leftover count are unrolled, so no loop is left in the code.
+  const int64_t k_est = j * kXcds / n_qb;
+  int k = (int)(k_est < n_units - 1 ? k_est : n_units - 1);
+#pragma unroll
+  for (int s = 0; s < kXcds; ++s)
+    if (k + 1 < n_units && prefix(k + 1) <= j) ++k;
+  int before = 0;  // sequences x' < x that take one of this group's leftover items
+#pragma unroll
+  for (int i = 0; i < kXcds - 1; ++i) before += (i < r && ((k * r + i) % kXcds) < x) ? 1 : 0;
+  *u_out = x * q + before + (int)(j - prefix(k));
+  return k;
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

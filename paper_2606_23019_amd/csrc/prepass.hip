@@ -69,7 +69,6 @@ __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
 }
 
 constexpr int kSchedThreads = 1024;
-constexpr int kXcds = 8;  // accelerator complex dies of an MI355X, one L2 each
 
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ counts,
                                                                   int B, int H, int n_qb,
@@ -114,27 +113,9 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
       __syncthreads();
     }
   }
-  // Position pos = x + 8 j is item j of sequence x.  Group of rank k gives
-  // sequence x the chunk of s(k, x) = q + e(k, x) items, e(k, x) = 1 for the
-  // r sequences (k r + i) mod 8, i < r.  prefix(k) counts the items of the
-  // ranks before k in sequence x: k q plus the t < k r with t = x (mod 8).
-  const int q = n_qb / kXcds;
-  const int r = n_qb - q * kXcds;
   for (int64_t pos = tid; pos < n_items; pos += kSchedThreads) {
-    const int x = (int)(pos % kXcds);
-    const int64_t j = pos / kXcds;
-    auto prefix = [&](int k) -> int64_t {
-      const int64_t t = (int64_t)k * r - x;
-      return (int64_t)k * q + (t > 0 ? (t + kXcds - 1) / kXcds : 0);
-    };
-    // average chunk n_qb / 8 gives the rank to within a few steps
-    const int64_t k_est = j * kXcds / n_qb;
-    int k = (int)(k_est < n_units - 1 ? k_est : n_units - 1);
-    while (k + 1 < n_units && prefix(k + 1) <= j) ++k;
-    while (k > 0 && prefix(k) > j) --k;
-    int before = 0;  // sequences x' < x that take one of this group's leftover items
-    for (int i = 0; i < r; ++i) before += ((k * r + i) % kXcds) < x;
-    const int u = x * q + before + (int)(j - prefix(k));
+    int u;
+    const int k = xcd_slice(pos, n_units, n_qb, &u);
     const int unit = (int)(keys[k] & 0xFFFFFFFFu);
     order[pos] = unit * n_qb + u;
   }
