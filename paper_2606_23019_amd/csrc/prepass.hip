@@ -82,10 +82,17 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
     for (int64_t i = tid; i < n_items; i += kSchedThreads) order[i] = (int32_t)i;
     return;
   }
-  for (int h = tid; h < H; h += kSchedThreads) {
+  // Per-head cost: `parts` threads per head each sum a strided share of the
+  // head's rows, then add it into LDS (few loads per thread instead of n_qb
+  // dependent-latency loads by one thread).
+  for (int h = tid; h < H; h += kSchedThreads) head_cost[h] = 0;
+  __syncthreads();
+  const int parts = H < kSchedThreads ? kSchedThreads / H : 1;
+  for (int w = tid; w < H * parts; w += kSchedThreads) {
+    const int h = w / parts;
     uint32_t c = 0;
-    for (int u = 0; u < n_qb; ++u) c += (uint32_t)counts[(int64_t)h * n_qb + u];
-    head_cost[h] = c;
+    for (int u = w - h * parts; u < n_qb; u += parts) c += (uint32_t)counts[(int64_t)h * n_qb + u];
+    atomicAdd(&head_cost[h], c);
   }
   int P = 1;
   while (P < n_units) P <<= 1;
