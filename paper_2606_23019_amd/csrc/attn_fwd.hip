@@ -5,8 +5,10 @@
 // query block's Compressed Row Mask row.  Each executed block is a dense
 // 128 x 128 (or 64 x 64) tile, so both contractions run on the matrix cores.
 //
-// Work item = (b, h, query block u); one workgroup per item, BQ / 32
-// wavefronts, each owning 32 query rows.  Per enabled key block kb:
+// Work item = (b, h, query block u), BQ / 32 wavefronts per item, each owning
+// 32 query rows.  128 x 128 tiles run two items per 8-wavefront workgroup in
+// ping-pong (bsattn_fwd_pp_kernel, described there); other tile shapes run
+// one item per workgroup (bsattn_fwd_kernel).  Per enabled key block kb:
 //
 //   1. the workgroup copies K[kb] and V[kb] (BK x D bf16, row-major) from
 //      global memory into LDS (16-byte chunks, XOR-swizzled per row);
@@ -24,7 +26,7 @@
 //      gfx950 transposing read ds_read_b64_tr_b16.
 //
 // Epilogue: out = O / l rounded to bf16, lse = (m + log2 l) ln 2.
-// The same kernel with DENSE = true is the maskless path (every key block).
+// The same kernels with DENSE = true are the maskless path (every key block).
 // Keys past N (ragged last block) are loaded as zeros and get -inf logits.
 
 #include <math.h>
@@ -377,14 +379,234 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
   }
 }
 
+
+// Two-item ping-pong kernel for 128 x 128 tiles.  An 8-wavefront workgroup
+// runs two items: wavefronts 0-3 and 4-7 form two groups, each with its own
+// K and V tiles in LDS (128 KB in all, so one workgroup per CU).  A group's
+// block loop alternates two phases separated by workgroup barriers:
+//   MFMA phase t:    P V of block t - 1, then S of block t (the MFMAs of a
+//                    step rotate over independent accumulators);
+//   softmax phase t: copies of V[t] and K[t + 1] issued, then the softmax of
+//                    block t; the phase ends once this group's copies landed.
+// The second group starts one barrier later, so on every SIMD one group's
+// softmax (vector ALU) runs beside the other group's MFMAs: gfx950 co-issues
+// the two from different wavefronts, not from one wavefront whose softmax
+// depends on its own S.  Both groups pass the same number of barriers: each
+// runs max(count0, count1) + 1 MFMA phases and max(count0, count1) softmax
+// phases, idle where its own item has no block, plus one offset barrier.
+// The two items are neighbours in one XCD's sequence of the schedule, so
+// they share most key blocks and have similar counts.
+template <int BQ, int BK, int D, bool DENSE>
+__global__ __launch_bounds__(2 * BQ / 32 * 64, 1) void bsattn_fwd_pp_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
+    const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
+    int N, int n_qb, int n_kb, float c_log2, int64_t sb, int64_t sh, int sn, int n_items) {
+  using T = Tile<BQ, BK, D>;
+  __shared__ __attribute__((aligned(1024))) __bf16 Ks_all[2][BK * D];
+  __shared__ __attribute__((aligned(1024))) __bf16 Vs_all[2][BK * D];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int grp = __builtin_amdgcn_readfirstlane(wave >> 2);
+  const int gwave = wave & 3;  // wavefront inside the group
+  const int half = lane >> 5;
+  const int l32 = lane & 31;
+  __bf16* Ks = Ks_all[grp];
+  __bf16* Vs = Vs_all[grp];
+
+  // Workgroup b on XCD b mod 8 takes items 2 (b / 8) and 2 (b / 8) + 1 of that
+  // XCD's sequence: the launch positions x + 8 j of the one-item layout.
+  auto item_at = [&](int g, int* cnt_out) -> int {
+    const int64_t pos = (int64_t)(blockIdx.x % kXcds) + kXcds * (2 * (int64_t)(blockIdx.x / kXcds) + g);
+    if (pos >= n_items) {
+      *cnt_out = 0;
+      return 0;
+    }
+    int it;
+    if (DENSE) {
+      int uu;
+      const int unit = xcd_slice(pos, n_items / n_qb, n_qb, &uu);
+      it = min(max(unit * n_qb + uu, 0), n_items - 1);
+    } else {
+      it = min(max(order[pos], 0), n_items - 1);
+    }
+    const int r = (it / n_qb) % H * n_qb + it % n_qb;
+    *cnt_out = DENSE ? n_kb : min(max(counts[r], 0), n_kb);
+    return it;
+  };
+  int cnt0, cnt1;
+  const int item0 = item_at(0, &cnt0);
+  const int item1 = item_at(1, &cnt1);
+  const int item = grp ? item1 : item0;
+  const int cnt = grp ? cnt1 : cnt0;
+  const int n_iter = max(cnt0, cnt1);
+  const bool has_item = (int64_t)(blockIdx.x % kXcds) + kXcds * (2 * (int64_t)(blockIdx.x / kXcds) + grp) < n_items;
+
+  const int bh = item / n_qb;
+  const int u = item - bh * n_qb;
+  const int h = bh % H;
+  const int row = h * n_qb + u;
+  const int32_t* list = DENSE ? nullptr : lists + (int64_t)row * n_kb;
+  auto kblk = [&](int t) { return DENSE ? t : min(max(list[t], 0), n_kb - 1); };
+  const int64_t base = (int64_t)(bh / H) * sb + (int64_t)h * sh;
+  const __bf16* Qb = Q + base;
+  const __bf16* Kb = K + base;
+  const __bf16* Vb = V + base;
+
+  const int gwave_u = __builtin_amdgcn_readfirstlane(gwave);
+  CopyPlan<T, D> cp;
+  cp.init(gwave_u, lane, sn);
+  if (cnt > 0) issue_tile_copy<T, BK, D>(Ks, Kb, kblk(0) * BK, N, sn, gwave_u, lane, cp);
+
+  const int qrow = u * BQ + gwave * 32 + l32;
+  bf16x8 qf[D / 16];
+#pragma unroll
+  for (int dc = 0; dc < D / 16; ++dc) {
+    if (has_item && qrow < N)
+      qf[dc] = *(const bf16x8*)(Qb + (int64_t)qrow * sn + dc * 16 + half * 8);
+    else
+      qf[dc] = bf16x8{};
+  }
+  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): Q and K[0] landed
+
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int dg = 0; dg < D / 32; ++dg) o[dg] = f32x16{};
+  float m_run = -INFINITY;
+  float l_run = 0.f;
+  const int g = lane >> 4;
+  const int j = lane & 15;
+  bf16x8 pf[BK / 16];
+#pragma unroll
+  for (int c = 0; c < BK / 16; ++c) pf[c] = bf16x8{};
+
+  if (grp == 1) barrier_lds_reads_done();  // the second group runs one phase behind
+  barrier_lds_reads_done();                // both groups' K[0] tiles are in LDS
+
+  for (int t = 0; t <= n_iter; ++t) {
+    // ---- MFMA phase: P V of block t - 1, then S of block t
+    if (t >= 1 && t - 1 < cnt) {
+#pragma unroll
+      for (int c = 0; c < BK / 16; ++c) {
+#pragma unroll
+        for (int dg = 0; dg < D / 32; ++dg) {
+          const int dd = dg * 32 + 16 * (g & 1) + (j & 3) * 4;
+          const int r0 = c * 16 + 8 * (g >> 1) + (j >> 2);
+          const int r1 = r0 + 4;
+          const bf16x4 lo = lds_read_tr16_b64(Vs + r0 * D + (((dd >> 3) ^ swz<D>(r0)) << 3) + (dd & 7));
+          const bf16x4 hi = lds_read_tr16_b64(Vs + r1 * D + (((dd >> 3) ^ swz<D>(r1)) << 3) + (dd & 7));
+          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          o[dg] = mfma32x32x16(a, pf[c], o[dg]);
+        }
+      }
+    }
+    f32x16 s[BK / 32];
+#pragma unroll
+    for (int kg = 0; kg < BK / 32; ++kg) s[kg] = f32x16{};
+    const bool do_s = t < cnt;
+    if (do_s) {
+#pragma unroll
+      for (int dc = 0; dc < D / 16; ++dc) {
+#pragma unroll
+        for (int kg = 0; kg < BK / 32; ++kg) {
+          const int kr = kg * 32 + key_of_row(l32);
+          const bf16x8 a = lds_read_b128(Ks + kr * D + (((2 * dc + half) ^ swz<D>(kr)) << 3));
+          s[kg] = mfma32x32x16(a, qf[dc], s[kg]);
+        }
+      }
+    }
+    barrier_lds_reads_done();  // this group's Ks and Vs are free
+    if (t == n_iter) break;
+
+    // ---- softmax phase of block t; copies of V[t] and K[t + 1]
+    if (do_s) {
+      const int key0 = kblk(t) * BK;
+      const bool more = t + 1 < cnt;
+      issue_tile_copy<T, BK, D>(Vs, Vb, key0, N, sn, gwave_u, lane, cp);
+      if (key0 + BK > N) {
+#pragma unroll
+        for (int kg = 0; kg < BK / 32; ++kg)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = key0 + kg * 32 + 16 * (i >> 3) + 8 * half + (i & 7);
+            if (key >= N) s[kg][i] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kg = 0; kg < BK / 32; ++kg)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kg][i]);
+      mx = fmaxf(mx, other_half(mx)) * c_log2;
+      if (more) issue_tile_copy<T, BK, D>(Ks, Kb, kblk(t + 1) * BK, N, sn, gwave_u, lane, cp);
+      const bool grow = mx > m_run;
+      if (__any(grow)) {
+        const float m_new = grow ? mx : m_run;
+        const float alpha = fast_exp2(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int dg = 0; dg < D / 32; ++dg) o[dg] *= alpha;
+      }
+      float lsum = 0.f;
+#pragma unroll
+      for (int kg = 0; kg < BK / 32; ++kg)
+#pragma unroll
+        for (int j8 = 0; j8 < 2; ++j8)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float p = fast_exp2(fmaf(s[kg][8 * j8 + e], c_log2, -m_run));
+            lsum += p;
+            pf[2 * kg + j8][e] = (__bf16)p;
+          }
+      l_run += lsum;
+    }
+    barrier_copies_landed<0>();  // this group's V[t] and K[t + 1] landed
+  }
+  if (grp == 0) barrier_lds_reads_done();  // matches the second group's extra barrier
+
+  const float l_tot = l_run + other_half(l_run);
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  const int lane_e = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int l32_e = lane_e & 31;
+  const int half_e = lane_e >> 5;
+  const int row0 = u * BQ + gwave_u * 32;
+  if (has_item && row0 + l32_e < N) {
+    if (half_e == 0)
+      LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
+    __bf16* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
+#pragma unroll
+    for (int dg = 0; dg < D / 32; ++dg)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const bf16x4 w = {(__bf16)(o[dg][4 * r4 + 0] * inv), (__bf16)(o[dg][4 * r4 + 1] * inv),
+                          (__bf16)(o[dg][4 * r4 + 2] * inv), (__bf16)(o[dg][4 * r4 + 3] * inv)};
+        *(bf16x4*)(orow + dg * 32 + 8 * r4 + 4 * half_e) = w;
+      }
+  }
+}
+
 template <int BQ, int BK, int D, bool DENSE>
 hipError_t launch_tile(const AttnArgs& a, hipStream_t stream) {
   const int64_t n_items = (int64_t)a.B * a.H * a.n_qb;
-  hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_items),
-                     dim3(Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
-                     (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
-                     (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
-                     a.sh, a.sn);
+  if constexpr (BQ == 128 && BK == 128) {
+    // two items per workgroup, in pairs of one XCD's sequence
+    const int64_t seq0 = (n_items + kXcds - 1) / kXcds;  // longest XCD sequence
+    const int64_t n_wg = kXcds * ((seq0 + 1) / 2);
+    hipLaunchKernelGGL((bsattn_fwd_pp_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_wg),
+                       dim3(2 * Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
+                       (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
+                       (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
+                       a.sh, a.sn, (int)n_items);
+  } else {
+    hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_items),
+                       dim3(Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
+                       (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
+                       (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
+                       a.sh, a.sn);
+  }
   return hipGetLastError();
 }
 
