@@ -119,6 +119,50 @@ def test_all_empty_mask_writes_zeros_and_neg_inf():
     assert (out2 == 0).all().item() and torch.isneginf(lse2).all().item()
 
 
+@pytest.mark.parametrize("B,H,N", [(1, 3, 1000), (3, 1, 640), (1, 5, 2048)])
+def test_pairs_with_unequal_counts_and_odd_item_counts(B, H, N):
+    """128 x 128 tiles run two neighbouring items per workgroup, in lockstep
+    over the longer item's blocks.  Rows alternate between empty, single,
+    dense and random so that paired items have very different counts; the
+    item totals are odd and n_qb is not a multiple of the 8 XCD slots.  The
+    one-shot call, the prepared call, a plan and the maskless path (for the
+    dense rows' heads) must all match the reference."""
+    from paper_2606_23019_amd import binding
+    torch = _torch()
+    blk, d = 128, 128
+    n = -(-N // blk)
+    rng = np.random.default_rng(N + H)
+    bm = np.zeros((H, n, n), dtype=bool)
+    for h in range(H):
+        for u in range(n):
+            kind = (u + h) % 4
+            if kind == 1:
+                bm[h, u, rng.integers(n)] = True
+            elif kind == 2:
+                bm[h, u, :] = True
+            elif kind == 3:
+                bm[h, u] = rng.random(n) < 0.4
+    packed = pack_rows(bm)
+    q, k, v = _rand_qkv(B, H, N, d, 51 + N)
+    ref_out, ref_lse = _full_reference(q, k, v, packed, blk, 1.0 / d ** 0.5)
+    out, lse = _run(q, k, v, packed, blk)
+    print(compare(out, lse, ref_out, ref_lse))
+    counts, lists = binding.mask_prepass(packed, H, n, n)
+    order = binding.schedule(counts, B, H, n)
+    o2, l2 = binding.bsattn_fwd_prepared(q, k, v, counts, lists, order, blk, blk)
+    plan = binding.Plan(packed, B, H, N, blk, blk)
+    o3, l3 = plan(q, k, v)
+    torch.cuda.synchronize()
+    plan.close()
+    assert torch.equal(o2.float().cpu(), torch.from_numpy(out)) and torch.equal(o3.float().cpu(), torch.from_numpy(out))
+    assert np.array_equal(l2.cpu().numpy(), lse, equal_nan=True) and np.array_equal(l3.cpu().numpy(), lse, equal_nan=True)
+    od, ld = binding.dense_attn_fwd(q, k, v, blk)
+    full = pack_rows(np.ones((H, n, n), dtype=bool))
+    rd_out, rd_lse = _full_reference(q, k, v, full, blk, 1.0 / d ** 0.5)
+    torch.cuda.synchronize()
+    print(compare(od.float().cpu().numpy(), ld.cpu().numpy(), rd_out, rd_lse))
+
+
 def test_large_logits_stay_finite():
     # q, k scaled by 4 give logits of std ~16: nearly one-hot rows, large maxima
     B, H, N, d, blk = 1, 2, 1024, 128, 128
