@@ -299,7 +299,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
     for (int kg = 0; kg < BK / 32; ++kg)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kg][i]);
-    mx = fmaxf(mx, other_half(mx)) * c_log2;
+    mx = pair_max(mx) * c_log2;
     if (more) issue_tile_slice<T, BK, D>(Ks, Kb, key1, N, sn, wave_u, lane, cp, 0, kL / 2);
     // Rescale only when some row's maximum grew.  Keeping the exact running
     // maximum (rather than a stale one) makes each row's largest probability
@@ -358,7 +358,7 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
   // Epilogue addresses are rebuilt from the wave-uniform row base and a lane
   // id recomputed here (mbcnt), so that nothing formed before the loop has to
   // stay live across it.
-  const float l_tot = l_run + other_half(l_run);
+  const float l_tot = pair_sum(l_run);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   const int lane_e = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int l32_e = lane_e & 31;
@@ -539,7 +539,7 @@ __global__ __launch_bounds__(2 * BQ / 32 * 64, 1) void bsattn_fwd_pp_kernel(
       for (int kg = 0; kg < BK / 32; ++kg)
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kg][i]);
-      mx = fmaxf(mx, other_half(mx)) * c_log2;
+      mx = pair_max(mx) * c_log2;
       if (more) issue_tile_copy<T, BK, D>(Ks, Kb, kblk(t + 1) * BK, N, sn, gwave_u, lane, cp);
       const bool grow = mx > m_run;
       if (__any(grow)) {
@@ -567,7 +567,7 @@ __global__ __launch_bounds__(2 * BQ / 32 * 64, 1) void bsattn_fwd_pp_kernel(
   }
   if (grp == 0) barrier_lds_reads_done();  // matches the second group's extra barrier
 
-  const float l_tot = l_run + other_half(l_run);
+  const float l_tot = pair_sum(l_run);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   const int lane_e = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int l32_e = lane_e & 31;

@@ -43,6 +43,22 @@ __device__ __forceinline__ void lds_write_b128(__bf16* p, u32x4 v) {
 // Value held by lane l ^ 32.
 __device__ __forceinline__ float other_half(float x) { return __shfl_xor(x, 32, 64); }
 
+// Max and sum of x over the lane pair (l, l ^ 32) with v_permlane32_swap,
+// which exchanges lanes 32..63 of its first operand with lanes 0..31 of its
+// second: with x in both, every lane ends up holding its own x and its
+// partner's, one in each result, and a symmetric operation on the two needs
+// no select.  Vector ALU only, unlike other_half (a ds_bpermute through the
+// LDS, which waits behind other wavefronts' LDS traffic).  Both results are
+// exactly those of x op other_half(x).
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Work layout for the XCDs.  Launch position pos runs on XCD pos mod 8 (the
 // dispatcher deals workgroups round-robin), and each XCD takes its positions
 // in increasing order.  Given n_units groups of n_qb items, ranked 0 ..
