@@ -6,9 +6,10 @@
 // 128 x 128 (or 64 x 64) tile, so both contractions run on the matrix cores.
 //
 // Work item = (b, h, query block u), BQ / 32 wavefronts per item, each owning
-// 32 query rows.  128 x 128 tiles run two items per 8-wavefront workgroup in
-// ping-pong (bsattn_fwd_pp_kernel, described there); other tile shapes run
-// one item per workgroup (bsattn_fwd_kernel).  Per enabled key block kb:
+// 32 query rows.  Items of 128 query rows, and the maskless path wherever
+// the tiles fit in LDS, run 2 (or 4) items per 8-wavefront workgroup in
+// ping-pong (bsattn_fwd_pp_kernel, described there); masked items of 64 rows
+// run one item per workgroup (bsattn_fwd_kernel).  Per enabled key block kb:
 //
 //   1. the workgroup copies K[kb] and V[kb] (BK x D bf16, row-major) from
 //      global memory into LDS (16-byte chunks, XOR-swizzled per row);
@@ -380,10 +381,29 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
 }
 
 
-// Two-item ping-pong kernel for 128 x 128 tiles.  An 8-wavefront workgroup
-// runs two items: wavefronts 0-3 and 4-7 form two groups, each with its own
-// K and V tiles in LDS (128 KB in all, so one workgroup per CU).  A group's
-// block loop alternates two phases separated by workgroup barriers:
+// Ping-pong workgroups: 8 wavefronts in two groups of 4; a group holds
+// 128 / BQ items (one of 128 query rows or two of 64), each item with its own
+// K and V tiles in LDS.  Used where those tiles fit the 160 KB of LDS.
+template <int BQ, int BK, int D>
+struct PingPong {
+  static constexpr int kItems = 8 / (BQ / 32);  // items per workgroup
+  static constexpr int kLdsBytes = kItems * 2 * BK * D * 2;
+  static constexpr bool kFits = kLdsBytes <= 160 * 1024;
+};
+
+// Where ping-pong is used: items of 128 query rows (two per workgroup), and
+// the maskless path wherever the tiles fit.  Masked items of 64 rows keep one
+// item per workgroup: four masked items in lockstep over the largest of their
+// counts measured 7-10 % slower than separate workgroups at densities of 0.1
+// and 0.25, while the maskless 64 x 64 path gained 5 %.
+template <int BQ, int BK, int D, bool DENSE>
+constexpr bool kUsePingPong = PingPong<BQ, BK, D>::kFits && (BQ == 128 || DENSE);
+
+// Ping-pong kernel.  An 8-wavefront workgroup runs 2 items of 128 query rows
+// (or 4 of 64): wavefronts 0-3 and 4-7 form two groups, each item with its
+// own K and V tiles in LDS (128 KB at 128 x 128, d = 128: one workgroup per
+// CU).  Every SIMD holds one wavefront of each group.  A group's block loop
+// alternates two phases separated by workgroup barriers:
 //   MFMA phase t:    P V of block t - 1, then S of block t (the MFMAs of a
 //                    step rotate over independent accumulators);
 //   softmax phase t: copies of V[t] and K[t + 1] issued, then the softmax of
@@ -392,34 +412,39 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
 // softmax (vector ALU) runs beside the other group's MFMAs: gfx950 co-issues
 // the two from different wavefronts, not from one wavefront whose softmax
 // depends on its own S.  Both groups pass the same number of barriers: each
-// runs max(count0, count1) + 1 MFMA phases and max(count0, count1) softmax
-// phases, idle where its own item has no block, plus one offset barrier.
-// The two items are neighbours in one XCD's sequence of the schedule, so
-// they share most key blocks and have similar counts.
+// runs max(counts) + 1 MFMA phases and max(counts) softmax phases over the
+// workgroup's items, idle where its own item has no block, plus one offset
+// barrier.  The items are neighbours in one XCD's sequence of the schedule,
+// so they share most key blocks and have similar counts.
 template <int BQ, int BK, int D, bool DENSE>
-__global__ __launch_bounds__(2 * BQ / 32 * 64, 1) void bsattn_fwd_pp_kernel(
+__global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
     int N, int n_qb, int n_kb, float c_log2, int64_t sb, int64_t sh, int sn, int n_items) {
   using T = Tile<BQ, BK, D>;
-  __shared__ __attribute__((aligned(1024))) __bf16 Ks_all[2][BK * D];
-  __shared__ __attribute__((aligned(1024))) __bf16 Vs_all[2][BK * D];
+  constexpr int kItems = PingPong<BQ, BK, D>::kItems;  // items per workgroup
+  __shared__ __attribute__((aligned(1024))) __bf16 Ks_all[kItems][BK * D];
+  __shared__ __attribute__((aligned(1024))) __bf16 Vs_all[kItems][BK * D];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int grp = __builtin_amdgcn_readfirstlane(wave >> 2);
-  const int gwave = wave & 3;  // wavefront inside the group
+  const int slot = __builtin_amdgcn_readfirstlane(wave / T::kWaves);  // this wave's item
+  const int gwave = wave % T::kWaves;  // wavefront inside its item
   const int half = lane >> 5;
   const int l32 = lane & 31;
-  __bf16* Ks = Ks_all[grp];
-  __bf16* Vs = Vs_all[grp];
+  __bf16* Ks = Ks_all[slot];
+  __bf16* Vs = Vs_all[slot];
 
-  // Workgroup b on XCD b mod 8 takes items 2 (b / 8) and 2 (b / 8) + 1 of that
-  // XCD's sequence: the launch positions x + 8 j of the one-item layout.
-  auto item_at = [&](int g, int* cnt_out) -> int {
-    const int64_t pos = (int64_t)(blockIdx.x % kXcds) + kXcds * (2 * (int64_t)(blockIdx.x / kXcds) + g);
+  // Workgroup b on XCD b mod 8 takes items kItems (b / 8) .. + kItems - 1 of
+  // that XCD's sequence: the launch positions x + 8 j of the one-item layout.
+  auto pos_of = [&](int sl) -> int64_t {
+    return (int64_t)(blockIdx.x % kXcds) + kXcds * (kItems * (int64_t)(blockIdx.x / kXcds) + sl);
+  };
+  auto item_at = [&](int sl, int* cnt_out) -> int {
+    const int64_t pos = pos_of(sl);
     if (pos >= n_items) {
       *cnt_out = 0;
       return 0;
@@ -436,13 +461,19 @@ __global__ __launch_bounds__(2 * BQ / 32 * 64, 1) void bsattn_fwd_pp_kernel(
     *cnt_out = DENSE ? n_kb : min(max(counts[r], 0), n_kb);
     return it;
   };
-  int cnt0, cnt1;
-  const int item0 = item_at(0, &cnt0);
-  const int item1 = item_at(1, &cnt1);
-  const int item = grp ? item1 : item0;
-  const int cnt = grp ? cnt1 : cnt0;
-  const int n_iter = max(cnt0, cnt1);
-  const bool has_item = (int64_t)(blockIdx.x % kXcds) + kXcds * (2 * (int64_t)(blockIdx.x / kXcds) + grp) < n_items;
+  // every item's count: all groups run max(counts) iterations
+  int item = 0, cnt = 0, n_iter = 0;
+#pragma unroll
+  for (int sl = 0; sl < kItems; ++sl) {
+    int c;
+    const int it = item_at(sl, &c);
+    n_iter = max(n_iter, c);
+    if (sl == slot) {
+      item = it;
+      cnt = c;
+    }
+  }
+  const bool has_item = pos_of(slot) < n_items;
 
   const int bh = item / n_qb;
   const int u = item - bh * n_qb;
@@ -591,12 +622,13 @@ __global__ __launch_bounds__(2 * BQ / 32 * 64, 1) void bsattn_fwd_pp_kernel(
 template <int BQ, int BK, int D, bool DENSE>
 hipError_t launch_tile(const AttnArgs& a, hipStream_t stream) {
   const int64_t n_items = (int64_t)a.B * a.H * a.n_qb;
-  if constexpr (BQ == 128 && BK == 128) {
-    // two items per workgroup, in pairs of one XCD's sequence
+  if constexpr (kUsePingPong<BQ, BK, D, DENSE>) {
+    // kItems consecutive items of one XCD's sequence per workgroup
+    constexpr int kItems = PingPong<BQ, BK, D>::kItems;
     const int64_t seq0 = (n_items + kXcds - 1) / kXcds;  // longest XCD sequence
-    const int64_t n_wg = kXcds * ((seq0 + 1) / 2);
+    const int64_t n_wg = kXcds * ((seq0 + kItems - 1) / kItems);
     hipLaunchKernelGGL((bsattn_fwd_pp_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_wg),
-                       dim3(2 * Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
+                       dim3(512), 0, stream, (const __bf16*)a.q,
                        (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
                        (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
                        a.sh, a.sn, (int)n_items);
