@@ -70,16 +70,27 @@ __device__ __forceinline__ float pair_sum(float x) {
 // positions).  Returns the rank k and writes the item's u.
 constexpr int kXcds = 8;  // accelerator complex dies of an MI355X, one L2 each
 
+// Items of sequence x in the groups of rank < k: k q plus the t < k r with
+// t = x (mod 8), where q = n_qb / 8 and r = n_qb mod 8.
+__device__ __forceinline__ int64_t xcd_prefix(int k, int x, int q, int r) {
+  const int64_t t = (int64_t)k * r - x;
+  return (int64_t)k * q + (t > 0 ? (t + kXcds - 1) / kXcds : 0);
+}
+
+// First u of chunk x of the group of rank k: x q plus the sequences x' < x
+// that take one of this group's leftover items.
+__device__ __forceinline__ int xcd_chunk_u0(int k, int x, int q, int r) {
+  int before = 0;
+#pragma unroll
+  for (int i = 0; i < kXcds - 1; ++i) before += (i < r && ((k * r + i) % kXcds) < x) ? 1 : 0;
+  return x * q + before;
+}
+
 __device__ __forceinline__ int xcd_slice(int64_t pos, int n_units, int n_qb, int* u_out) {
   const int q = n_qb / kXcds;
   const int r = n_qb - q * kXcds;
   const int x = (int)(pos % kXcds);
   const int64_t j = pos / kXcds;
-  // items of sequence x in the groups of rank < k: k q plus the t < k r with t = x (mod 8)
-  auto prefix = [&](int k) -> int64_t {
-    const int64_t t = (int64_t)k * r - x;
-    return (int64_t)k * q + (t > 0 ? (t + kXcds - 1) / kXcds : 0);
-  };
   // k0 = floor(8 j / n_qb) has prefix(k0) <= j (k0 q + ceil(k0 r / 8) <= j
   // since 8 k0 q + k0 r <= 8 j), and the rank is at most 1 + 7 / n_qb above
   // it, so a fixed number of forward steps finds it; the steps and the
@@ -88,11 +99,8 @@ __device__ __forceinline__ int xcd_slice(int64_t pos, int n_units, int n_qb, int
   int k = (int)(k_est < n_units - 1 ? k_est : n_units - 1);
 #pragma unroll
   for (int s = 0; s < kXcds; ++s)
-    if (k + 1 < n_units && prefix(k + 1) <= j) ++k;
-  int before = 0;  // sequences x' < x that take one of this group's leftover items
-#pragma unroll
-  for (int i = 0; i < kXcds - 1; ++i) before += (i < r && ((k * r + i) % kXcds) < x) ? 1 : 0;
-  *u_out = x * q + before + (int)(j - prefix(k));
+    if (k + 1 < n_units && xcd_prefix(k + 1, x, q, r) <= j) ++k;
+  *u_out = xcd_chunk_u0(k, x, q, r) + (int)(j - xcd_prefix(k, x, q, r));
   return k;
 }
 

@@ -69,6 +69,7 @@ __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
 }
 
 constexpr int kSchedThreads = 1024;
+constexpr int kSchedWindow = 64;  // one wavefront
 
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ counts,
                                                                   int B, int H, int n_qb,
@@ -120,11 +121,47 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
       __syncthreads();
     }
   }
-  for (int64_t pos = tid; pos < n_items; pos += kSchedThreads) {
-    int u;
-    const int k = xcd_slice(pos, n_units, n_qb, &u);
+  // Chunk (x, k) of sequence x holds the group of rank k's query blocks
+  // u0 .. u0 + len - 1 at sequence places prefix(k) .. + len - 1.  The
+  // attention kernel runs neighbouring places of a sequence side by side
+  // (two per ping-pong workgroup, in lockstep over the larger count), so each
+  // chunk is cut into windows of up to 64 places, and inside a window the
+  // query blocks are placed by enabled-block count: decreasing in even
+  // windows of the sequence, increasing in odd ones, so that a pair which
+  // straddles two windows also meets counts from the same end.  The window
+  // still holds the same consecutive query blocks, so the L2 reuse of their
+  // K/V tiles is unchanged.  One wavefront per window: lane t holds query
+  // block u0 + t, ranks it among the window (ties by u) and scatters it.
+  const int q = n_qb / kXcds;
+  const int r = n_qb - q * kXcds;
+  const int win_per_chunk = (q + 1 + kSchedWindow - 1) / kSchedWindow;
+  const int64_t n_windows = (int64_t)kXcds * n_units * win_per_chunk;
+  const int lane = tid & 63;
+  for (int64_t w = tid >> 6; w < n_windows; w += kSchedThreads / 64) {
+    const int x = (int)(w % kXcds);
+    const int64_t rest = w / kXcds;
+    const int k = (int)(rest / win_per_chunk);
+    const int wi = (int)(rest - (int64_t)k * win_per_chunk);
+    const int64_t j0 = xcd_prefix(k, x, q, r);
+    const int len = (int)(xcd_prefix(k + 1, x, q, r) - j0);
+    const int L = min(kSchedWindow, len - wi * kSchedWindow);
+    if (L <= 0) continue;  // uniform per wavefront
+    const int u0 = xcd_chunk_u0(k, x, q, r) + wi * kSchedWindow;
     const int unit = (int)(keys[k] & 0xFFFFFFFFu);
-    order[pos] = unit * n_qb + u;
+    const int c = lane < L ? counts[(int64_t)(unit % H) * n_qb + u0 + lane] : 0;
+    int rank = 0;  // window members placed before this one
+    for (int i = 0; i < L; ++i) {
+      const int ci = __builtin_amdgcn_readlane(c, i);
+      rank += (ci > c || (ci == c && i < lane)) ? 1 : 0;
+    }
+    // windows of sequence x before this one: chunks of q places have
+    // ceil(q / 64) windows, chunks of q + 1 one more when 64 divides q
+    const int64_t before =
+        (int64_t)k * ((q + kSchedWindow - 1) / kSchedWindow) +
+        (q % kSchedWindow == 0 ? j0 - (int64_t)k * q : 0) + wi;
+    const int t = (before & 1) ? L - 1 - rank : rank;
+    if (lane < L)
+      order[x + kXcds * (j0 + (int64_t)wi * kSchedWindow + t)] = unit * n_qb + u0 + lane;
   }
 }
 

@@ -76,19 +76,30 @@ def test_prepass_ignores_bits_past_last_block():
         assert np.array_equal(a[r, :n[r]], b[r, :n[r]])
 
 
-def _xcd_order(units_sorted, n_qb, xcds=8):
+def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
     """The documented order, built literally: sequence x gets chunk x of every
     group (groups heaviest first), chunks of n_qb // 8 items plus one leftover
     item for the sequences (k r + i) mod 8, i < r = n_qb mod 8, of the group of
-    rank k; position x + 8 j holds item j of sequence x."""
+    rank k.  Each chunk is cut into windows of up to 64 consecutive query
+    blocks; the i-th window of a sequence holds its query blocks by decreasing
+    enabled-block count (ties by u) when i is even, the reverse when i is odd.
+    Position x + 8 j holds item j of sequence x.  row_counts[unit][u] is the
+    enabled-block count of query block u of group unit."""
     q, r = divmod(n_qb, xcds)
     seqs = [[] for _ in range(xcds)]
+    n_win = [0] * xcds
     for k, unit in enumerate(units_sorted):
         extra = {(k * r + i) % xcds for i in range(r)}
         start = 0
         for x in range(xcds):
             size = q + (1 if x in extra else 0)
-            seqs[x].extend(unit * n_qb + u for u in range(start, start + size))
+            for w0 in range(start, start + size, win):
+                us = sorted(range(w0, min(w0 + win, start + size)),
+                            key=lambda u: (-row_counts[unit][u], u))
+                if n_win[x] % 2:
+                    us.reverse()
+                n_win[x] += 1
+                seqs[x].extend(unit * n_qb + u for u in us)
             start += size
     order = [None] * (len(units_sorted) * n_qb)
     for x, seq in enumerate(seqs):
@@ -97,7 +108,7 @@ def _xcd_order(units_sorted, n_qb, xcds=8):
     return order
 
 
-@pytest.mark.parametrize("n", [48, 45, 3, 256])
+@pytest.mark.parametrize("n", [48, 45, 3, 256, 515, 1100])
 def test_schedule_is_an_xcd_sliced_heaviest_first_permutation(n):
     from paper_2606_23019_amd import binding
     rng = np.random.default_rng(11 + n)
@@ -113,9 +124,10 @@ def test_schedule_is_an_xcd_sliced_heaviest_first_permutation(n):
         assert sorted(order.tolist()) == list(range(B * H * n))
         cost = bm.reshape(H, -1).sum(axis=1)
         units = sorted(range(B * H), key=lambda x: (-cost[x % H], x))
-        assert order.tolist() == _xcd_order(units, n)
+        row_counts = [bm[x % H].sum(axis=1) for x in range(B * H)]
+        assert order.tolist() == _xcd_order(units, n, row_counts)
         # every XCD slot (positions = x mod 8) visits the groups heaviest first,
-        # each group's items in one ascending run of consecutive query blocks
+        # each group's items in one run that holds consecutive query blocks
         for x in range(8):
             seq = order[x::8]
             groups = seq // n
@@ -124,5 +136,5 @@ def test_schedule_is_an_xcd_sliced_heaviest_first_permutation(n):
             c = [cost[g % H] for g in runs]
             assert all(a >= b for a, b in zip(c, c[1:]))
             for g in set(runs):
-                us = seq[groups == g] % n
+                us = np.sort(seq[groups == g] % n)
                 assert np.all(np.diff(us) == 1)
