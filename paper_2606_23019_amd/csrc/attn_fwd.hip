@@ -105,74 +105,85 @@ __device__ __forceinline__ void copy16_to_lds(uint32_t lds_byte_addr, const void
                : "memory");
 }
 
-// Per-lane byte offsets of a tile copy: lane l of load i writes the 16-byte
-// LDS chunk 64 (i + kLoadsPerWave * wave) + l, i.e. row r and physical chunk p;
-// the XOR swizzle is applied by reading source chunk p ^ swz(r).  Source rows
-// are sn elements apart (d for [B][H][N][d] tensors, H d for [B][N][H][d]).
+// Per-lane byte offsets of a tile copy.  Lane l of load i writes the 16-byte
+// LDS chunk 64 (i + kLoadsPerWave * wave) + l, i.e. row r = R (kLoadsPerWave
+// wave + i) + l / C and physical chunk p = l mod C (C chunks per row, R = 64 / C
+// rows per load); the XOR swizzle is applied by reading source chunk
+// p ^ swz(r).  Source rows are sn elements apart (d for [B][H][N][d] tensors,
+// H d for [B][N][H][d]).  The swizzle depends on r mod 16 only, so the lane's
+// part of the offset repeats with period 4 in the load index n = kLoadsPerWave
+// wave + i, and the rest, R n sn elements, is uniform over the wavefront:
+// a plan holds 4 lane offsets, and each load adds its uniform row offset to
+// the scalar base address.  (Every real row is congruent mod 16 to the row
+// used for its swizzle: R (n - n mod 4) is a multiple of 16.)
 template <typename T, int D>
 struct CopyPlan {
-  uint32_t off[T::kLoadsPerWave];  // byte offset inside the source tile
+  static constexpr int kRowsPerLoad = 64 / T::kChunksPerRow;
+  uint32_t lane_off[4];  // byte offset of the lane's chunk for loads with n mod 4 = m
   __device__ __forceinline__ void init(int wave, int lane, int sn) {
 #pragma unroll
-    for (int i = 0; i < T::kLoadsPerWave; ++i) {
-      const int idx = (wave * T::kLoadsPerWave + i) * 64 + lane;
-      const int r = idx / T::kChunksPerRow;
-      const int p = idx % T::kChunksPerRow;
-      off[i] = (uint32_t)(r * sn + ((p ^ swz<D>(r)) << 3)) * 2u;
+    for (int j = 0; j < 4; ++j) {
+      const int m = (wave * T::kLoadsPerWave + j) & 3;  // n mod 4 of load j, j + 4, ...
+      const int lr = lane / T::kChunksPerRow;
+      const int p = lane % T::kChunksPerRow;
+      const int r = m * kRowsPerLoad + lr;  // row relative to load n - n mod 4
+      lane_off[j] = (uint32_t)(r * sn + ((p ^ swz<D>(r)) << 3)) * 2u;
     }
+  }
+  // wavefront-uniform byte offset of load i: rows R (n - n mod 4)
+  __device__ __forceinline__ static int64_t row_off(int wave, int i, int sn) {
+    const int n = wave * T::kLoadsPerWave + i;
+    return (int64_t)((n & ~3) * kRowsPerLoad) * sn * 2;
   }
 };
 
-// Start copying rows key0 .. key0 + BK - 1 (rows sn elements apart) into an
-// LDS tile with global_load_lds_dwordx4 (no registers; completion is tracked
-// by vmcnt).  In a ragged last block, rows past N repeat row N - 1: finite
-// values whose logits are masked and whose probabilities are exactly zero.
-template <typename T, int BK, int D>
-__device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, int key0, int N,
-                                                int sn, int wave_u, int lane,
-                                                const CopyPlan<T, D>& cp) {
-  const __bf16* tile = src + (int64_t)key0 * sn;
-  const uint32_t lds0 =
-      (uint32_t)(uintptr_t)(SA_LDS void*)lds + (uint32_t)(wave_u * T::kLoadsPerWave * 1024);
-  if (key0 + BK <= N) {
-#pragma unroll
-    for (int i = 0; i < T::kLoadsPerWave; ++i) copy16_to_lds(lds0 + i * 1024, tile, cp.off[i]);
-  } else {
-    const int last = N - 1 - key0;  // last real row of this tile
-#pragma unroll
-    for (int i = 0; i < T::kLoadsPerWave; ++i) {
-      const int idx = (wave_u * T::kLoadsPerWave + i) * 64 + lane;
-      const int r = idx / T::kChunksPerRow;
-      const int p = idx % T::kChunksPerRow;
-      const uint32_t o = (uint32_t)(min(r, last) * sn + ((p ^ swz<D>(r)) << 3)) * 2u;
-      copy16_to_lds(lds0 + i * 1024, tile, o);
-    }
-  }
-}
-
-// Loads i0 .. i0 + count - 1 of a tile copy (count and i0 are compile-time
-// constants wherever this is inlined into an unrolled loop).
+// Loads i0 .. i0 + count - 1 of a copy of rows key0 .. key0 + BK - 1 (rows sn
+// elements apart) into an LDS tile with global_load_lds_dwordx4 (no
+// registers; completion is tracked by vmcnt).  count and i0 are compile-time
+// constants wherever this is inlined into an unrolled loop.  In a ragged last
+// block, rows past N repeat row N - 1: finite values whose logits are masked
+// and whose probabilities are exactly zero.
 template <typename T, int BK, int D>
 __device__ __forceinline__ void issue_tile_slice(__bf16* lds, const __bf16* src, int key0, int N,
                                                  int sn, int wave_u, int lane,
                                                  const CopyPlan<T, D>& cp, int i0, int count) {
-  const __bf16* tile = src + (int64_t)key0 * sn;
+  const char* tile = (const char*)(src + (int64_t)key0 * sn);
   const uint32_t lds0 =
       (uint32_t)(uintptr_t)(SA_LDS void*)lds + (uint32_t)(wave_u * T::kLoadsPerWave * 1024);
   if (key0 + BK <= N) {
 #pragma unroll
-    for (int i = i0; i < i0 + count; ++i) copy16_to_lds(lds0 + i * 1024, tile, cp.off[i]);
+    for (int i = i0; i < i0 + count; ++i)
+      copy16_to_lds(lds0 + i * 1024, tile + CopyPlan<T, D>::row_off(wave_u, i, sn),
+                    cp.lane_off[i & 3]);
   } else {
-    const int last = N - 1 - key0;
+    // Row R n + lr of the tile is read from row min(R n + lr, last), addressed
+    // from the tile start: lane_off covers rows R (n mod 4) + lr, so the rows
+    // still to add are min(R (n - n mod 4), last - R (n mod 4) - lr), which is
+    // negative when the clamped row lies below row R (n - n mod 4).  The sum
+    // is taken mod 2^32 and equals the true offset, which is non-negative and
+    // inside the tile.  (Adding a negative row count to the uniform base of a
+    // full-tile load instead would wrap the 32-bit lane offset.)
+    const int last = N - 1 - key0;  // last real row of this tile
+    int lr = lane / T::kChunksPerRow;
+    // opaque to the optimiser: keeps the per-load row sums below from being
+    // hoisted out of the block loop, where they would hold 4 registers
+    asm volatile("" : "+v"(lr));
 #pragma unroll
     for (int i = i0; i < i0 + count; ++i) {
-      const int idx = (wave_u * T::kLoadsPerWave + i) * 64 + lane;
-      const int r = idx / T::kChunksPerRow;
-      const int p = idx % T::kChunksPerRow;
-      const uint32_t o = (uint32_t)(min(r, last) * sn + ((p ^ swz<D>(r)) << 3)) * 2u;
-      copy16_to_lds(lds0 + i * 1024, tile, o);
+      const int n = wave_u * T::kLoadsPerWave + i;
+      constexpr int R = CopyPlan<T, D>::kRowsPerLoad;
+      const int rows = min((n & ~3) * R, last - (n & 3) * R - lr);
+      copy16_to_lds(lds0 + i * 1024, tile, cp.lane_off[i & 3] + (uint32_t)(rows * sn) * 2u);
     }
   }
+}
+
+// A whole tile copy.
+template <typename T, int BK, int D>
+__device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, int key0, int N,
+                                                int sn, int wave_u, int lane,
+                                                const CopyPlan<T, D>& cp) {
+  issue_tile_slice<T, BK, D>(lds, src, key0, N, sn, wave_u, lane, cp, 0, T::kLoadsPerWave);
 }
 
 // DENSE = true is the maskless path: every key block 0 .. n_kb - 1 is enabled
