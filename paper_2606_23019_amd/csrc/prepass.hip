@@ -22,7 +22,10 @@
 // structured masks, so their K/V tiles are reused from its L2, and every XCD
 // gets an equal slice of every group, so the load stays balanced.  One
 // workgroup computes each group's total enabled blocks, sorts the groups
-// with a bitonic network in LDS and writes the order.
+// with a bitonic network in LDS and writes the order, each chunk in
+// ascending u; a second kernel then sorts every window of up to 64 places of
+// a chunk by enabled-block count, so that the items the attention kernel
+// runs side by side have similar counts.
 
 #include "device_common.h"
 #include "launch.h"
@@ -121,48 +124,76 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
       __syncthreads();
     }
   }
-  // Chunk (x, k) of sequence x holds the group of rank k's query blocks
-  // u0 .. u0 + len - 1 at sequence places prefix(k) .. + len - 1.  The
-  // attention kernel runs neighbouring places of a sequence side by side
-  // (two per ping-pong workgroup, in lockstep over the larger count), so each
-  // chunk is cut into windows of up to 64 places, and inside a window the
-  // query blocks are placed by enabled-block count: decreasing in even
-  // windows of the sequence, increasing in odd ones, so that a pair which
-  // straddles two windows also meets counts from the same end.  The window
-  // still holds the same consecutive query blocks, so the L2 reuse of their
-  // K/V tiles is unchanged.  One wavefront per window: lane t holds query
-  // block u0 + t, ranks it among the window (ties by u) and scatters it.
+  // Ascending u inside each chunk here; window_sort_kernel then reorders
+  // each window of a chunk by count.
+  for (int64_t pos = tid; pos < n_items; pos += kSchedThreads) {
+    int u;
+    const int k = xcd_slice(pos, n_units, n_qb, &u);
+    const int unit = (int)(keys[k] & 0xFFFFFFFFu);
+    order[pos] = unit * n_qb + u;
+  }
+}
+
+// Chunk (x, k) of sequence x holds the group of rank k's query blocks
+// u0 .. u0 + len - 1 at sequence places prefix(k) .. + len - 1.  The attention
+// kernel runs neighbouring places of a sequence side by side (two per
+// ping-pong workgroup, in lockstep over the larger count), so each chunk is
+// cut into windows of up to 64 places, and inside a window the query blocks
+// are placed by enabled-block count: decreasing in even windows of the
+// sequence, increasing in odd ones, so that a pair which straddles two
+// windows also meets counts from the same end.  The window still holds the
+// same consecutive query blocks, so the L2 reuse of their K/V tiles is
+// unchanged.  The places of window (x, k, wi) depend on k only, not on which
+// group has rank k, so this runs after schedule_kernel on the order it wrote,
+// one wavefront per window across the whole chip: lane t reads the item at
+// the window's place t, keys it as (count << 6) | (63 - t) (distinct keys,
+// larger for larger counts and, among equal counts, for smaller t), counts
+// the larger keys of the window from a key row in LDS, and writes the item
+// back at its rank's place.  Each window's places are read and written by its
+// own wavefront only, so the permutation happens in place.
+constexpr int kWindowSortWaves = 4;
+
+__global__ __launch_bounds__(64 * kWindowSortWaves) void window_sort_kernel(
+    const int32_t* __restrict__ counts, int H, int n_qb, int n_units, int32_t* __restrict__ order) {
+  __shared__ __attribute__((aligned(16))) int32_t key_rows[kWindowSortWaves][kSchedWindow];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int q = n_qb / kXcds;
   const int r = n_qb - q * kXcds;
   const int win_per_chunk = (q + 1 + kSchedWindow - 1) / kSchedWindow;
-  const int64_t n_windows = (int64_t)kXcds * n_units * win_per_chunk;
-  const int lane = tid & 63;
-  for (int64_t w = tid >> 6; w < n_windows; w += kSchedThreads / 64) {
-    const int x = (int)(w % kXcds);
-    const int64_t rest = w / kXcds;
-    const int k = (int)(rest / win_per_chunk);
-    const int wi = (int)(rest - (int64_t)k * win_per_chunk);
-    const int64_t j0 = xcd_prefix(k, x, q, r);
-    const int len = (int)(xcd_prefix(k + 1, x, q, r) - j0);
-    const int L = min(kSchedWindow, len - wi * kSchedWindow);
-    if (L <= 0) continue;  // uniform per wavefront
-    const int u0 = xcd_chunk_u0(k, x, q, r) + wi * kSchedWindow;
-    const int unit = (int)(keys[k] & 0xFFFFFFFFu);
-    const int c = lane < L ? counts[(int64_t)(unit % H) * n_qb + u0 + lane] : 0;
-    int rank = 0;  // window members placed before this one
-    for (int i = 0; i < L; ++i) {
-      const int ci = __builtin_amdgcn_readlane(c, i);
-      rank += (ci > c || (ci == c && i < lane)) ? 1 : 0;
-    }
-    // windows of sequence x before this one: chunks of q places have
-    // ceil(q / 64) windows, chunks of q + 1 one more when 64 divides q
-    const int64_t before =
-        (int64_t)k * ((q + kSchedWindow - 1) / kSchedWindow) +
-        (q % kSchedWindow == 0 ? j0 - (int64_t)k * q : 0) + wi;
-    const int t = (before & 1) ? L - 1 - rank : rank;
-    if (lane < L)
-      order[x + kXcds * (j0 + (int64_t)wi * kSchedWindow + t)] = unit * n_qb + u0 + lane;
+  const int64_t w = (int64_t)blockIdx.x * kWindowSortWaves + wave;
+  if (w >= (int64_t)kXcds * n_units * win_per_chunk) return;  // uniform per wavefront
+  const int x = (int)(w % kXcds);
+  const int rest = (int)(w / kXcds);
+  const int k = rest / win_per_chunk;
+  const int wi = rest - k * win_per_chunk;
+  const int64_t j0 = xcd_prefix(k, x, q, r);
+  const int len = (int)(xcd_prefix(k + 1, x, q, r) - j0);
+  const int L = min(kSchedWindow, len - wi * kSchedWindow);
+  if (L <= 0) return;  // uniform per wavefront
+  const int64_t first = j0 + (int64_t)wi * kSchedWindow;  // the window's first place
+  int item = 0, key = -1;  // lanes past the window hold -1, below every key
+  if (lane < L) {
+    item = order[x + kXcds * (first + lane)];
+    const int64_t row = (int64_t)(item / n_qb % H) * n_qb + item % n_qb;
+    key = (min(max(counts[row], 0), (1 << 24) - 1) << 6) | (63 - lane);
   }
+  int32_t* key_row = key_rows[wave];
+  key_row[lane] = key;
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the wavefront's keys are in LDS
+  int rank = 0;  // window members placed before this one
+#pragma unroll 4
+  for (int i = 0; i < L; i += 4) {  // keys past L (up to a multiple of 4) are -1
+    const i32x4 kv = *(const SA_LDS i32x4*)(key_row + i);
+    rank += (kv[0] > key ? 1 : 0) + (kv[1] > key ? 1 : 0) + (kv[2] > key ? 1 : 0) +
+            (kv[3] > key ? 1 : 0);
+  }
+  // windows of sequence x before this one: chunks of q places have
+  // ceil(q / 64) windows, chunks of q + 1 one more when 64 divides q
+  const int64_t before = (int64_t)k * ((q + kSchedWindow - 1) / kSchedWindow) +
+                         (q % kSchedWindow == 0 ? j0 - (int64_t)k * q : 0) + wi;
+  const int t = (before & 1) ? L - 1 - rank : rank;
+  if (lane < L) order[x + kXcds * (first + t)] = item;
 }
 
 }  // namespace
@@ -181,6 +212,14 @@ hipError_t launch_schedule(const int32_t* counts, int B, int H, int n_qb, int32_
                            hipStream_t stream) {
   hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), 0, stream, counts, B, H, n_qb,
                      order);
+  const int n_units = B * H;
+  if (n_units <= kScheduleMaxUnits) {  // otherwise the order is the identity
+    const int q = n_qb / kXcds;
+    const int64_t n_windows = (int64_t)kXcds * n_units * ((q + 1 + kSchedWindow - 1) / kSchedWindow);
+    const int64_t grid = (n_windows + kWindowSortWaves - 1) / kWindowSortWaves;
+    hipLaunchKernelGGL(window_sort_kernel, dim3((unsigned)grid), dim3(64 * kWindowSortWaves), 0,
+                       stream, counts, H, n_qb, n_units, order);
+  }
   return hipGetLastError();
 }
 

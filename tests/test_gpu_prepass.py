@@ -108,7 +108,8 @@ def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
     return order
 
 
-@pytest.mark.parametrize("n", [48, 45, 3, 256, 515, 1100])
+# 4100: 7 x 4100 row counts exceed what the schedule stages in LDS (24576)
+@pytest.mark.parametrize("n", [48, 45, 3, 256, 515, 1100, 4100])
 def test_schedule_is_an_xcd_sliced_heaviest_first_permutation(n):
     from paper_2606_23019_amd import binding
     rng = np.random.default_rng(11 + n)
