@@ -454,44 +454,50 @@ __global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
   auto pos_of = [&](int sl) -> int64_t {
     return (int64_t)(blockIdx.x % kXcds) + kXcds * (kItems * (int64_t)(blockIdx.x / kXcds) + sl);
   };
-  auto item_at = [&](int sl, int* cnt_out) -> int {
-    const int64_t pos = pos_of(sl);
-    if (pos >= n_items) {
-      *cnt_out = 0;
-      return 0;
-    }
-    int it;
+  // The look-ups are branch-free (positions clamped, validity applied after
+  // the loads), so that the scalar loads of all items go out together:
+  // every order entry, then every count and this item's first key block, in
+  // two rounds of memory latency instead of one chain per item.
+  int it_of[kItems];
+#pragma unroll
+  for (int sl = 0; sl < kItems; ++sl) {
+    const int64_t pos = min(pos_of(sl), (int64_t)n_items - 1);
     if (DENSE) {
       int uu;
       const int unit = xcd_slice(pos, n_items / n_qb, n_qb, &uu);
-      it = min(max(unit * n_qb + uu, 0), n_items - 1);
+      it_of[sl] = min(max(unit * n_qb + uu, 0), n_items - 1);
     } else {
-      it = min(max(order[pos], 0), n_items - 1);
-    }
-    const int r = (it / n_qb) % H * n_qb + it % n_qb;
-    *cnt_out = DENSE ? n_kb : min(max(counts[r], 0), n_kb);
-    return it;
-  };
-  // every item's count: all groups run max(counts) iterations
-  int item = 0, cnt = 0, n_iter = 0;
-#pragma unroll
-  for (int sl = 0; sl < kItems; ++sl) {
-    int c;
-    const int it = item_at(sl, &c);
-    n_iter = max(n_iter, c);
-    if (sl == slot) {
-      item = it;
-      cnt = c;
+      it_of[sl] = order[pos];
     }
   }
-  const bool has_item = pos_of(slot) < n_items;
-
+  __builtin_amdgcn_sched_barrier(0);  // all order loads issued before any is used
+  int c_of[kItems];
+  int item = 0;
+#pragma unroll
+  for (int sl = 0; sl < kItems; ++sl) {
+    const int it = min(max(it_of[sl], 0), n_items - 1);
+    c_of[sl] = DENSE ? n_kb : counts[(it / n_qb) % H * n_qb + it % n_qb];
+    if (sl == slot) item = it;
+  }
   const int bh = item / n_qb;
   const int u = item - bh * n_qb;
   const int h = bh % H;
   const int row = h * n_qb + u;
   const int32_t* list = DENSE ? nullptr : lists + (int64_t)row * n_kb;
   auto kblk = [&](int t) { return DENSE ? t : min(max(list[t], 0), n_kb - 1); };
+  int first = kblk(0);  // in range for every row (n_kb >= 1): read before cnt is known
+  asm volatile("" : "+s"(first));     // keeps that load here, not inside the cnt > 0 branch
+  __builtin_amdgcn_sched_barrier(0);  // counts and the first key block issued together
+  // every item's count: all groups run max(counts) iterations
+  int cnt = 0, n_iter = 0;
+#pragma unroll
+  for (int sl = 0; sl < kItems; ++sl) {
+    const int c = pos_of(sl) < n_items ? min(max(c_of[sl], 0), n_kb) : 0;
+    n_iter = max(n_iter, c);
+    if (sl == slot) cnt = c;
+  }
+  const bool has_item = pos_of(slot) < n_items;
+
   const int64_t base = (int64_t)(bh / H) * sb + (int64_t)h * sh;
   const __bf16* Qb = Q + base;
   const __bf16* Kb = K + base;
@@ -500,7 +506,7 @@ __global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
   const int gwave_u = __builtin_amdgcn_readfirstlane(gwave);
   CopyPlan<T, D> cp;
   cp.init(gwave_u, lane, sn);
-  if (cnt > 0) issue_tile_copy<T, BK, D>(Ks, Kb, kblk(0) * BK, N, sn, gwave_u, lane, cp);
+  if (cnt > 0) issue_tile_copy<T, BK, D>(Ks, Kb, first * BK, N, sn, gwave_u, lane, cp);
 
   const int qrow = u * BQ + gwave * 32 + l32;
   bf16x8 qf[D / 16];
