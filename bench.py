@@ -477,6 +477,40 @@ def reference_gemm(attention_tflops, n=8192, reps=10):
             "attention_kernel_frac_of_it": round(attention_tflops / tflops, 4)}
 
 
+def mfma_microbench(attention_tflops, iters=100000, reps=3):
+    """The sustained bf16 MFMA rate of this GPU: the probe kernel of
+    libsa_mfma_peak.so (one workgroup of 8 wavefronts per CU, four independent
+    32x32x16 accumulators per wavefront, register operands holding random bf16
+    values), timed with events over ~50 ms launches, so the clock settles where
+    the power limit puts it."""
+    import ctypes
+    import torch
+    from paper_2606_23019_amd import build as _b
+    if not os.path.exists(_b.MFMA_PEAK_PATH):
+        return None
+    lib = ctypes.CDLL(_b.MFMA_PEAK_PATH)
+    lib.sa_mfma_peak.restype = ctypes.c_int
+    lib.sa_mfma_peak.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                 ctypes.c_void_p]
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    g = torch.Generator(device="cuda")
+    g.manual_seed(78)
+    src = torch.randn((2 * 4 * 64 * 8,), generator=g, device="cuda").to(torch.bfloat16)
+    out = torch.empty((n_cu * 8 * 64,), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def launch():
+        if lib.sa_mfma_peak(src.data_ptr(), out.data_ptr(), n_cu, iters, stream) != 0:
+            raise RuntimeError("sa_mfma_peak launch failed")
+    launch()
+    ms = _events_time(launch, reps)
+    tflops = n_cu * 8 * iters * 16 * 32768 / (ms * 1e-3) / 1e12
+    return {"what": "v_mfma_f32_32x32x16_bf16 on random register operands, 8 wavefronts per CU "
+                    "x %d CUs, %.1f ms per launch" % (n_cu, ms),
+            "tflops": round(tflops, 1), "frac_of_2500": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "attention_kernel_frac_of_it": round(attention_tflops / tflops, 4)}
+
+
 COPY_BYTES = 1 << 30
 
 
@@ -578,6 +612,7 @@ def main():
     torch.cuda.synchronize()
     parity = parity_spot_check(case)
     gemm = reference_gemm(achieved)
+    mfma_probe = mfma_microbench(achieved)
 
     traffic = traffic_record()
     rec = {
@@ -610,6 +645,7 @@ def main():
         "crm_overhead_at_density_1": round(ms_dense / ms_maskless - 1.0, 4),
         "parity_spot_check": parity,
         "reference_gemm": gemm,
+        "mfma_microbench": mfma_probe,
         "roofline": {
             "bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),

@@ -18,6 +18,9 @@ LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "prepass.hip", "mask_inst.hip", "fidelity.hip", "resize.hip", "attn_fwd.hip"]
+# sustained MFMA rate probe, a measurement helper of bench.py (not in the C ABI)
+MFMA_PEAK_SOURCES = ["mfma_peak.hip"]
+MFMA_PEAK_PATH = os.path.join(PKG_DIR, "libsa_mfma_peak.so")
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=" + ARCH,
@@ -37,10 +40,9 @@ def hipcc():
     raise RuntimeError("hipcc not found: the HIP library cannot be built")
 
 
-def build(verbose=False):
-    """Compile all sources into LIB_PATH (atomically replaced); return the path."""
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB_PATH + ".tmp%d" % os.getpid()
+def _compile(sources, lib_path, verbose):
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = lib_path + ".tmp%d" % os.getpid()
     cmd = [hipcc()] + HIPCC_FLAGS + ["-I", os.path.join(ROOT, "include"), "-o", tmp] + srcs
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -53,7 +55,16 @@ def build(verbose=False):
         raise RuntimeError("hipcc failed (%d):\n%s" % (r.returncode, out))
     if verbose and out.strip():
         print(out)
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, lib_path)
+    return lib_path
+
+
+def build(verbose=False):
+    """Compile all sources into LIB_PATH (atomically replaced), and the MFMA-rate
+    probe the benchmark reads its measured peak from into MFMA_PEAK_PATH; return
+    LIB_PATH."""
+    _compile(SOURCES, LIB_PATH, verbose)
+    _compile(MFMA_PEAK_SOURCES, MFMA_PEAK_PATH, verbose)
     return LIB_PATH
 
 
