@@ -139,3 +139,16 @@ def test_schedule_is_an_xcd_sliced_heaviest_first_permutation(n):
             for g in set(runs):
                 us = np.sort(seq[groups == g] % n)
                 assert np.all(np.diff(us) == 1)
+
+
+@pytest.mark.parametrize("B,H", [(1, 4097), (2, 2049)])
+def test_schedule_is_the_identity_beyond_4096_groups(B, H):
+    # more than 4096 (b, h) groups: no ranking and no window sort, items in index order
+    from paper_2606_23019_amd import binding
+    n = 3
+    rng = np.random.default_rng(5 + B)
+    bm = rng.random((H, n, n)) < 0.5
+    bm[:, np.arange(n), np.arange(n)] = True
+    counts, _ = binding.mask_prepass(pack_rows(bm), H, n, n)
+    order = binding.schedule(counts, B, H, n).cpu().numpy()
+    assert order.tolist() == list(range(B * H * n))
