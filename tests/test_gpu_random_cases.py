@@ -1,0 +1,91 @@
+"""Seeded random shapes through the C ABI against the float64 reference.
+
+Each case draws B, H, N (ragged tails included), d, blk_q and blk_k
+independently, a density (empty rows and an all-empty head included), a
+per-case input scale, and the tensor layout, then checks the one-shot call
+and the static-mask plan: both against the reference, and the plan bit for bit
+against the one-shot call.  The draws cover the kernels' instantiations (the
+two-item ping-pong kernel for 128-row items, the one-item kernel for 64-row
+items) together with the schedule's window sort at small n_qb.  Input scales
+reach 2, where rows are nearly one-hot and |out| reaches 4-8: the out bound
+per element takes the bf16 rounding of P into account (helpers.compare,
+pv_abs).
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from helpers import compare, to_bits
+from workloads import pack_rows
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 24
+
+
+def _case(seed):
+    rng = np.random.default_rng(9100 + seed)
+    B = int(rng.integers(1, 4))
+    H = int(rng.integers(1, 6))
+    blk_q = int(rng.choice([64, 128]))
+    blk_k = int(rng.choice([64, 128]))
+    N = int(rng.integers(1, 2600)) if seed % 4 else int(rng.choice([128, 256, 1024, 2048]))
+    d = int(rng.choice([64, 128]))
+    rho = float(rng.choice([0.0, 0.05, 0.2, 0.5, 0.9, 1.0]))
+    layout = "bnhd" if seed % 3 == 0 else "bhnd"
+    scale_in = float(rng.uniform(0.5, 2.0))
+    return dict(B=B, H=H, N=N, d=d, blk_q=blk_q, blk_k=blk_k, rho=rho, layout=layout,
+                scale_in=scale_in, seed=seed)
+
+
+def _mask(c, rng):
+    n_qb, n_kb = -(-c["N"] // c["blk_q"]), -(-c["N"] // c["blk_k"])
+    bm = rng.random((c["H"], n_qb, n_kb)) < c["rho"]
+    if c["rho"] > 0:
+        # the diagonal block of most rows, so that few rows are empty
+        keep = rng.random((c["H"], n_qb)) < 0.9
+        for u in range(n_qb):
+            v = min(u * c["blk_q"] // c["blk_k"], n_kb - 1)
+            bm[:, u, v] |= keep[:, u]
+    if c["H"] > 1 and c["seed"] % 5 == 0:
+        bm[-1] = False                     # one head without any enabled block
+    return bm, pack_rows(bm)
+
+
+@pytest.mark.parametrize("seed", list(range(N_CASES)))
+def test_random_case(seed):
+    import torch
+    from paper_2606_23019_amd import binding
+    c = _case(seed)
+    rng = np.random.default_rng(9200 + seed)
+    bm, packed = _mask(c, rng)
+    print("case", c, "enabled blocks", int(bm.sum()), flush=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(9300 + seed)
+    shape = (c["B"], c["H"], c["N"], c["d"])
+    q, k, v = ((torch.randn(shape, generator=g, device="cuda") * c["scale_in"]).to(torch.bfloat16)
+               for _ in range(3))
+    scale = 1.0 / c["d"] ** 0.5
+    qb, kb, vb = to_bits(q), to_bits(k), to_bits(v)
+    ref_out, ref_lse = oracle.attention(qb, kb, vb, packed, c["blk_q"], c["blk_k"], scale)
+    # the same weights on |v| (sign bit cleared): bounds the effect of rounding P to bf16
+    pv_abs, _ = oracle.attention(qb, kb, vb & np.uint16(0x7FFF), packed, c["blk_q"], c["blk_k"],
+                                 scale)
+    if c["layout"] == "bnhd":
+        qt, kt, vt = (t.transpose(1, 2).contiguous() for t in (q, k, v))
+        out_t, lse = binding.bsattn_fwd_bnhd(qt, kt, vt, packed, c["blk_q"], c["blk_k"], scale)
+        out = out_t.transpose(1, 2)
+    else:
+        out, lse = binding.bsattn_fwd(q, k, v, packed, c["blk_q"], c["blk_k"], scale)
+    torch.cuda.synchronize()
+    compare(out.float().cpu().numpy(), lse.cpu().numpy(), ref_out, ref_lse, pv_abs=pv_abs)
+    if c["layout"] == "bhnd":
+        plan = binding.Plan(packed, c["B"], c["H"], c["N"], c["blk_q"], c["blk_k"])
+        try:
+            assert plan.executed_blocks == c["B"] * int(bm.sum())
+            out_p, lse_p = plan(q, k, v, scale)
+            torch.cuda.synchronize()
+            assert torch.equal(out_p, out) and torch.equal(lse_p, lse)
+        finally:
+            plan.close()
