@@ -74,6 +74,20 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v,
                          int B, int H, int N, int d, int blk_q, int blk_k,
                          float scale, void* stream);
 
+/*
+ * One-shot forward pass as sa_bsattn_fwd, with out in float32 (contiguous
+ * [B][H][N][d], 16-byte aligned; q, k, v stay bf16 and lse float32): the
+ * kernel's fp32 accumulator divided by the row sum, with no bf16 rounding of
+ * the result.  For callers that need the 2e-2 absolute bound on out even
+ * where |out| >= 8, where half a bf16 ulp alone is 0.03.  The arithmetic up
+ * to that last step is the same as sa_bsattn_fwd's, so the bf16 out of
+ * sa_bsattn_fwd is the round-to-nearest-even of this out, and lse is bit for
+ * bit the same.  Costs 2 more bytes of HBM writes per output element.
+ */
+SA_API int sa_bsattn_fwd_f32out(const void* q, const void* k, const void* v,
+                                const uint64_t* mask_bits, float* out, float* lse, int B, int H,
+                                int N, int d, int blk_q, int blk_k, float scale, void* stream);
+
 /* Tensor layouts accepted by sa_bsattn_fwd_layout. */
 #define SA_LAYOUT_BHND 0 /* [B][H][N][d]: heads outermost (the other entry points) */
 #define SA_LAYOUT_BNHD 1 /* [B][N][H][d]: tokens outermost, as a DiT's projections emit */
@@ -246,6 +260,10 @@ SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
  */
 SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v,
                               void* out, float* lse, int d, float scale, void* stream);
+
+/* sa_bsattn_fwd_plan with a float32 out, as sa_bsattn_fwd_f32out. */
+SA_API int sa_bsattn_fwd_plan_f32out(sa_plan_t plan, const void* q, const void* k, const void* v,
+                                     float* out, float* lse, int d, float scale, void* stream);
 
 /* Total executed (b, h, u, v) blocks of the plan: B * sum of all row counts. */
 SA_API int sa_bsattn_plan_stats(sa_plan_t plan, int64_t* executed_blocks);

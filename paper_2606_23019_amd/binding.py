@@ -35,6 +35,8 @@ SIGNATURES = {
     "sa_bsattn_fwd_prepared": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
     "sa_bsattn_plan_create": (_I, [_P, _I, _I, _I, _I, _I, _P, ctypes.POINTER(_P)]),
     "sa_bsattn_fwd_plan": (_I, [_P, _P, _P, _P, _P, _P, _I, _F, _P]),
+    "sa_bsattn_fwd_f32out": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
+    "sa_bsattn_fwd_plan_f32out": (_I, [_P, _P, _P, _P, _P, _P, _I, _F, _P]),
     "sa_bsattn_plan_stats": (_I, [_P, ctypes.POINTER(ctypes.c_int64)]),
     "sa_bsattn_plan_destroy": (_I, [_P]),
     "sa_dense_attn_fwd": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _P]),
@@ -117,10 +119,10 @@ def _same_shape(ref, others, names):
               % (n, tuple(t.shape), tuple(ref.shape)))
 
 
-def _outputs(q, out, lse, lse_shape):
+def _outputs(q, out, lse, lse_shape, out_dtype=None):
     torch = _torch()
     if out is None:
-        out = torch.empty_like(q)
+        out = torch.empty_like(q, dtype=out_dtype or q.dtype)
     _need(tuple(out.shape) == tuple(q.shape), "out must have the shape of q")
     if lse is None:
         lse = torch.empty(lse_shape, dtype=torch.float32, device=q.device)
@@ -150,12 +152,7 @@ def mask_to_device(mask_bits, device="cuda"):
     return torch.from_numpy(m.copy()).to(device)
 
 
-def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None, stream=None):
-    """One-shot forward: ``sa_bsattn_fwd``.  q, k, v: bf16 [B, H, N, d] on the GPU.
-
-    mask_bits: int64/uint64 device tensor (or numpy uint64) [H, n_qb, W].
-    Returns (out bf16 [B, H, N, d], lse float32 [B, H, N]).
-    """
+def _fwd_oneshot(fn, out_dtype, q, k, v, mask_bits, blk_q, blk_k, scale, out, lse, stream):
     torch = _torch()
     lib = load()
     B, H, N, d = q.shape
@@ -166,14 +163,31 @@ def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
     if m.dtype == torch.uint64:
         m = m.view(torch.int64)
     _mask_words(m, H, -(-N // int(blk_q)), -(-N // int(blk_k)))
-    out, lse = _outputs(q, out, lse, (B, H, N))
-    st = lib.sa_bsattn_fwd(
+    out, lse = _outputs(q, out, lse, (B, H, N), out_dtype)
+    st = getattr(lib, fn)(
         _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
         _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(m, torch.int64, "mask_bits"),
-        _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
+        _dev_ptr(out, out_dtype, "out"), _dev_ptr(lse, torch.float32, "lse"),
         B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
-    _check("sa_bsattn_fwd", st)
+    _check(fn, st)
     return out, lse
+
+
+def bsattn_fwd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None, stream=None):
+    """One-shot forward: ``sa_bsattn_fwd``.  q, k, v: bf16 [B, H, N, d] on the GPU.
+
+    mask_bits: int64/uint64 device tensor (or numpy uint64) [H, n_qb, W].
+    Returns (out bf16 [B, H, N, d], lse float32 [B, H, N]).
+    """
+    return _fwd_oneshot("sa_bsattn_fwd", _torch().bfloat16, q, k, v, mask_bits, blk_q, blk_k,
+                        scale, out, lse, stream)
+
+
+def bsattn_fwd_f32out(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
+                      stream=None):
+    """``sa_bsattn_fwd_f32out``: as ``bsattn_fwd`` with out float32 [B, H, N, d]."""
+    return _fwd_oneshot("sa_bsattn_fwd_f32out", _torch().float32, q, k, v, mask_bits, blk_q,
+                        blk_k, scale, out, lse, stream)
 
 
 def bsattn_fwd_bnhd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=None,
@@ -376,7 +390,7 @@ class Plan:
         _check("sa_bsattn_plan_stats", self._lib.sa_bsattn_plan_stats(self._h, ctypes.byref(n)))
         return n.value
 
-    def __call__(self, q, k, v, scale=None, out=None, lse=None, stream=None):
+    def _fwd(self, fn, out_dtype, q, k, v, scale, out, lse, stream):
         torch = _torch()
         B, H, N, d = q.shape
         if (B, H, N) != (self.B, self.H, self.N):
@@ -384,13 +398,23 @@ class Plan:
         _same_shape(q, (k, v), ("k", "v"))
         if scale is None:
             scale = 1.0 / float(d) ** 0.5
-        out, lse = _outputs(q, out, lse, (B, H, N))
-        st = self._lib.sa_bsattn_fwd_plan(
+        out, lse = _outputs(q, out, lse, (B, H, N), out_dtype)
+        st = getattr(self._lib, fn)(
             self._h, _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
-            _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, torch.bfloat16, "out"),
+            _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, out_dtype, "out"),
             _dev_ptr(lse, torch.float32, "lse"), d, float(scale), _stream(stream))
-        _check("sa_bsattn_fwd_plan", st)
+        _check(fn, st)
         return out, lse
+
+    def __call__(self, q, k, v, scale=None, out=None, lse=None, stream=None):
+        """``sa_bsattn_fwd_plan``: (out bf16 [B, H, N, d], lse float32 [B, H, N])."""
+        return self._fwd("sa_bsattn_fwd_plan", _torch().bfloat16, q, k, v, scale, out, lse,
+                         stream)
+
+    def fwd_f32out(self, q, k, v, scale=None, out=None, lse=None, stream=None):
+        """``sa_bsattn_fwd_plan_f32out``: as the call, with out float32."""
+        return self._fwd("sa_bsattn_fwd_plan_f32out", _torch().float32, q, k, v, scale, out, lse,
+                         stream)
 
     def close(self):
         if getattr(self, "_h", None):

@@ -45,7 +45,8 @@ int check_shape(int B, int H, int N, int blk_q, int blk_k, Dims* dims) {
 }
 
 int check_tensors(const void* q, const void* k, const void* v, const void* mask_bits, size_t mask_words,
-                  const void* out, const float* lse, int B, int H, int N, int d, float scale) {
+                  const void* out, const float* lse, int B, int H, int N, int d, float scale,
+                  size_t out_elem = 2) {
   if (d != 64 && d != 128) return SA_ERR_UNSUPPORTED;
   if (!(scale > 0.f) || !isfinite(scale)) return SA_ERR_INVALID_ARG;
   if (!q || !k || !v || !out || !lse) return SA_ERR_INVALID_ARG;
@@ -53,16 +54,17 @@ int check_tensors(const void* q, const void* k, const void* v, const void* mask_
       !aligned(lse, 4))
     return SA_ERR_INVALID_ARG;
   const size_t tensor_bytes = (size_t)B * H * N * d * 2;
+  const size_t out_bytes = (size_t)B * H * N * d * out_elem;
   const size_t lse_bytes = (size_t)B * H * N * 4;
   const size_t mask_bytes = (size_t)mask_words * 8;
   const void* ins[4] = {q, k, v, mask_bits};
   const size_t in_bytes[4] = {tensor_bytes, tensor_bytes, tensor_bytes, mask_bytes};
   for (int i = 0; i < 4; ++i) {
     if (!ins[i]) continue;
-    if (overlap(out, tensor_bytes, ins[i], in_bytes[i])) return SA_ERR_INVALID_ARG;
+    if (overlap(out, out_bytes, ins[i], in_bytes[i])) return SA_ERR_INVALID_ARG;
     if (overlap(lse, lse_bytes, ins[i], in_bytes[i])) return SA_ERR_INVALID_ARG;
   }
-  if (overlap(out, tensor_bytes, lse, lse_bytes)) return SA_ERR_INVALID_ARG;
+  if (overlap(out, out_bytes, lse, lse_bytes)) return SA_ERR_INVALID_ARG;
   return SA_OK;
 }
 
@@ -178,33 +180,46 @@ SA_API int sa_schedule(const int32_t* counts, int B, int H, int n_qb, int32_t* o
   return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
-SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
-                                  const int32_t* counts, const int32_t* lists,
-                                  const int32_t* order, void* out, float* lse, int B, int H, int N,
-                                  int d, int blk_q, int blk_k, float scale, void* stream) {
+// Attention kernel alone on a prepared pre-pass and schedule; out is bf16 or,
+// with out_f32, fp32.
+static int fwd_prepared(const void* q, const void* k, const void* v, const int32_t* counts,
+                        const int32_t* lists, const int32_t* order, void* out, float* lse, int B,
+                        int H, int N, int d, int blk_q, int blk_k, float scale, bool out_f32,
+                        void* stream) {
   Dims dm;
   int st = check_shape(B, H, N, blk_q, blk_k, &dm);
   if (st != SA_OK) return st;
-  st = check_tensors(q, k, v, nullptr, 0, out, lse, B, H, N, d, scale);
+  st = check_tensors(q, k, v, nullptr, 0, out, lse, B, H, N, d, scale, out_f32 ? 4 : 2);
   if (st != SA_OK) return st;
   if (!counts || !lists || !order) return SA_ERR_INVALID_ARG;
   if (!aligned(counts, 4) || !aligned(lists, 4) || !aligned(order, 4)) return SA_ERR_INVALID_ARG;
   sa::AttnArgs a{q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k,
                  dm.n_qb, dm.n_kb, scale,
                  (int64_t)H * N * d, (int64_t)N * d, d};
+  a.out_f32 = out_f32;
   return sa::launch_attention(a, (hipStream_t)stream) == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
-// One-shot forward for either tensor layout (strides in elements).
+SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
+                                  const int32_t* counts, const int32_t* lists,
+                                  const int32_t* order, void* out, float* lse, int B, int H, int N,
+                                  int d, int blk_q, int blk_k, float scale, void* stream) {
+  return fwd_prepared(q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k, scale,
+                      false, stream);
+}
+
+// One-shot forward for either tensor layout (strides in elements); out is
+// bf16 or, with out_f32, fp32.
 static int fwd_oneshot(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
                        void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
-                       float scale, int layout, void* stream) {
+                       float scale, int layout, bool out_f32, void* stream) {
   Dims dm;
   int st = check_shape(B, H, N, blk_q, blk_k, &dm);
   if (st != SA_OK) return st;
   if (!mask_bits || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
   if (layout != SA_LAYOUT_BHND && layout != SA_LAYOUT_BNHD) return SA_ERR_INVALID_ARG;
-  st = check_tensors(q, k, v, mask_bits, (size_t)H * dm.n_qb * dm.W, out, lse, B, H, N, d, scale);
+  st = check_tensors(q, k, v, mask_bits, (size_t)H * dm.n_qb * dm.W, out, lse, B, H, N, d, scale,
+                     out_f32 ? 4 : 2);
   if (st != SA_OK) return st;
   const bool bnhd = layout == SA_LAYOUT_BNHD;
   const int sn = bnhd ? H * d : d;
@@ -225,6 +240,7 @@ static int fwd_oneshot(const void* q, const void* k, const void* v, const uint64
     sa::AttnArgs a{q, k, v, counts, lists, order, out, lse, B, H, N, d, blk_q, blk_k,
                    dm.n_qb, dm.n_kb, scale,
                    (int64_t)H * N * d, bnhd ? (int64_t)d : (int64_t)N * d, sn};
+    a.out_f32 = out_f32;
     e = sa::launch_attention(a, s);
   }
   const hipError_t ef = hipFreeAsync(ws, s);
@@ -235,14 +251,22 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint
                          void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
                          float scale, void* stream) {
   return fwd_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale,
-                     SA_LAYOUT_BHND, stream);
+                     SA_LAYOUT_BHND, false, stream);
+}
+
+SA_API int sa_bsattn_fwd_f32out(const void* q, const void* k, const void* v,
+                                const uint64_t* mask_bits, float* out, float* lse, int B, int H,
+                                int N, int d, int blk_q, int blk_k, float scale, void* stream) {
+  return fwd_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale,
+                     SA_LAYOUT_BHND, true, stream);
 }
 
 SA_API int sa_bsattn_fwd_layout(const void* q, const void* k, const void* v,
                                 const uint64_t* mask_bits, void* out, float* lse, int B, int H,
                                 int N, int d, int blk_q, int blk_k, float scale, int layout,
                                 void* stream) {
-  return fwd_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale, layout, stream);
+  return fwd_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale, layout, false,
+                     stream);
 }
 
 SA_API int sa_dense_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
@@ -338,14 +362,24 @@ SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
   return SA_OK;
 }
 
-SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v,
-                              void* out, float* lse, int d, float scale, void* stream) {
+static int fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v, void* out,
+                    float* lse, int d, float scale, bool out_f32, void* stream) {
   if (!plan) return SA_ERR_INVALID_ARG;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return SA_ERR_HIP;
   if (dev != plan->device) return SA_ERR_INVALID_ARG;  // the plan's buffers live on its device
-  return sa_bsattn_fwd_prepared(q, k, v, plan->counts, plan->lists, plan->order, out, lse, plan->B,
-                                plan->H, plan->N, d, plan->blk_q, plan->blk_k, scale, stream);
+  return fwd_prepared(q, k, v, plan->counts, plan->lists, plan->order, out, lse, plan->B, plan->H,
+                      plan->N, d, plan->blk_q, plan->blk_k, scale, out_f32, stream);
+}
+
+SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, const void* v,
+                              void* out, float* lse, int d, float scale, void* stream) {
+  return fwd_plan(plan, q, k, v, out, lse, d, scale, false, stream);
+}
+
+SA_API int sa_bsattn_fwd_plan_f32out(sa_plan_t plan, const void* q, const void* k, const void* v,
+                                     float* out, float* lse, int d, float scale, void* stream) {
+  return fwd_plan(plan, q, k, v, out, lse, d, scale, true, stream);
 }
 
 SA_API int sa_bsattn_plan_stats(sa_plan_t plan, int64_t* executed_blocks) {

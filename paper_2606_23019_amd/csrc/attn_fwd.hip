@@ -26,7 +26,8 @@
 //      in an order that makes this so -- and V^T comes from LDS through the
 //      gfx950 transposing read ds_read_b64_tr_b16.
 //
-// Epilogue: out = O / l rounded to bf16, lse = (m + log2 l) ln 2.
+// Epilogue: out = O / l rounded to bf16 (or kept in fp32 for the fp32-output
+// entry points), lse = (m + log2 l) ln 2.
 // The same kernels with DENSE = true are the maskless path (every key block).
 // Keys past N (ragged last block) are loaded as zeros and get -inf logits.
 
@@ -186,6 +187,14 @@ __device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, 
   issue_tile_slice<T, BK, D>(lds, src, key0, N, sn, wave_u, lane, cp, 0, T::kLoadsPerWave);
 }
 
+// Four consecutive outputs of a row: bf16 (round to nearest even) or fp32.
+__device__ __forceinline__ void store_out4(__bf16* p, float a, float b, float c, float d) {
+  *(bf16x4*)p = bf16x4{(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+}
+__device__ __forceinline__ void store_out4(float* p, float a, float b, float c, float d) {
+  *(f32x4*)p = f32x4{a, b, c, d};
+}
+
 // DENSE = true is the maskless path: every key block 0 .. n_kb - 1 is enabled
 // (counts, lists and order unused) and the items are laid out for the XCDs
 // as the schedule lays them out, with the (b, h) groups in index order.
@@ -195,11 +204,11 @@ __device__ __forceinline__ void issue_tile_copy(__bf16* lds, const __bf16* src, 
 template <int BQ, int BK, int D>
 constexpr int kWavesPerSimd = (BQ == 64 && BK == 128 && D == 128) ? 1 : 2;
 
-template <int BQ, int BK, int D, bool DENSE>
+template <int BQ, int BK, int D, bool DENSE, typename OutT>
 __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsattn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
-    const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
+    const int32_t* __restrict__ order, OutT* __restrict__ O, float* __restrict__ LSE, int H,
     int N, int n_qb, int n_kb, float c_log2, int64_t sb, int64_t sh, int sn) {
   using T = Tile<BQ, BK, D>;
   constexpr int kL = T::kLoadsPerWave;
@@ -379,15 +388,13 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
   if (row0 + l32_e < N) {
     if (half_e == 0)
       LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
-    __bf16* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
+    OutT* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
 #pragma unroll
     for (int dg = 0; dg < D / 32; ++dg)
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const bf16x4 w = {(__bf16)(o[dg][4 * r4 + 0] * inv), (__bf16)(o[dg][4 * r4 + 1] * inv),
-                          (__bf16)(o[dg][4 * r4 + 2] * inv), (__bf16)(o[dg][4 * r4 + 3] * inv)};
-        *(bf16x4*)(orow + dg * 32 + 8 * r4 + 4 * half_e) = w;
-      }
+      for (int r4 = 0; r4 < 4; ++r4)
+        store_out4(orow + dg * 32 + 8 * r4 + 4 * half_e, o[dg][4 * r4 + 0] * inv,
+                   o[dg][4 * r4 + 1] * inv, o[dg][4 * r4 + 2] * inv, o[dg][4 * r4 + 3] * inv);
   }
 }
 
@@ -427,11 +434,11 @@ constexpr bool kUsePingPong = PingPong<BQ, BK, D>::kFits && (BQ == 128 || DENSE)
 // workgroup's items, idle where its own item has no block, plus one offset
 // barrier.  The items are neighbours in one XCD's sequence of the schedule,
 // so they share most key blocks and have similar counts.
-template <int BQ, int BK, int D, bool DENSE>
+template <int BQ, int BK, int D, bool DENSE, typename OutT>
 __global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const int32_t* __restrict__ counts, const int32_t* __restrict__ lists,
-    const int32_t* __restrict__ order, __bf16* __restrict__ O, float* __restrict__ LSE, int H,
+    const int32_t* __restrict__ order, OutT* __restrict__ O, float* __restrict__ LSE, int H,
     int N, int n_qb, int n_kb, float c_log2, int64_t sb, int64_t sh, int sn, int n_items) {
   using T = Tile<BQ, BK, D>;
   constexpr int kItems = PingPong<BQ, BK, D>::kItems;  // items per workgroup
@@ -624,19 +631,17 @@ __global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
   if (has_item && row0 + l32_e < N) {
     if (half_e == 0)
       LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
-    __bf16* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
+    OutT* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
 #pragma unroll
     for (int dg = 0; dg < D / 32; ++dg)
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const bf16x4 w = {(__bf16)(o[dg][4 * r4 + 0] * inv), (__bf16)(o[dg][4 * r4 + 1] * inv),
-                          (__bf16)(o[dg][4 * r4 + 2] * inv), (__bf16)(o[dg][4 * r4 + 3] * inv)};
-        *(bf16x4*)(orow + dg * 32 + 8 * r4 + 4 * half_e) = w;
-      }
+      for (int r4 = 0; r4 < 4; ++r4)
+        store_out4(orow + dg * 32 + 8 * r4 + 4 * half_e, o[dg][4 * r4 + 0] * inv,
+                   o[dg][4 * r4 + 1] * inv, o[dg][4 * r4 + 2] * inv, o[dg][4 * r4 + 3] * inv);
   }
 }
 
-template <int BQ, int BK, int D, bool DENSE>
+template <int BQ, int BK, int D, bool DENSE, typename OutT>
 hipError_t launch_tile(const AttnArgs& a, hipStream_t stream) {
   const int64_t n_items = (int64_t)a.B * a.H * a.n_qb;
   if constexpr (kUsePingPong<BQ, BK, D, DENSE>) {
@@ -644,45 +649,46 @@ hipError_t launch_tile(const AttnArgs& a, hipStream_t stream) {
     constexpr int kItems = PingPong<BQ, BK, D>::kItems;
     const int64_t seq0 = (n_items + kXcds - 1) / kXcds;  // longest XCD sequence
     const int64_t n_wg = kXcds * ((seq0 + kItems - 1) / kItems);
-    hipLaunchKernelGGL((bsattn_fwd_pp_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_wg),
+    hipLaunchKernelGGL((bsattn_fwd_pp_kernel<BQ, BK, D, DENSE, OutT>), dim3((unsigned)n_wg),
                        dim3(512), 0, stream, (const __bf16*)a.q,
                        (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
-                       (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
+                       (OutT*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
                        a.sh, a.sn, (int)n_items);
   } else {
-    hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D, DENSE>), dim3((unsigned)n_items),
+    hipLaunchKernelGGL((bsattn_fwd_kernel<BQ, BK, D, DENSE, OutT>), dim3((unsigned)n_items),
                        dim3(Tile<BQ, BK, D>::kThreads), 0, stream, (const __bf16*)a.q,
                        (const __bf16*)a.k, (const __bf16*)a.v, a.counts, a.lists, a.order,
-                       (__bf16*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
+                       (OutT*)a.out, a.lse, a.H, a.N, a.n_qb, a.n_kb, a.scale * kLog2e, a.sb,
                        a.sh, a.sn);
   }
   return hipGetLastError();
 }
 
-template <int BQ, int BK, bool DENSE>
+template <int BQ, int BK, bool DENSE, typename OutT>
 hipError_t launch_d(const AttnArgs& a, hipStream_t stream) {
-  if (a.d == 128) return launch_tile<BQ, BK, 128, DENSE>(a, stream);
-  if (a.d == 64) return launch_tile<BQ, BK, 64, DENSE>(a, stream);
+  if (a.d == 128) return launch_tile<BQ, BK, 128, DENSE, OutT>(a, stream);
+  if (a.d == 64) return launch_tile<BQ, BK, 64, DENSE, OutT>(a, stream);
   return hipErrorInvalidValue;
 }
 
-template <bool DENSE>
+template <bool DENSE, typename OutT>
 hipError_t launch_any(const AttnArgs& a, hipStream_t stream) {
-  if (a.blk_q == 128 && a.blk_k == 128) return launch_d<128, 128, DENSE>(a, stream);
-  if (a.blk_q == 64 && a.blk_k == 64) return launch_d<64, 64, DENSE>(a, stream);
-  if (a.blk_q == 128 && a.blk_k == 64) return launch_d<128, 64, DENSE>(a, stream);
-  if (a.blk_q == 64 && a.blk_k == 128) return launch_d<64, 128, DENSE>(a, stream);
+  if (a.blk_q == 128 && a.blk_k == 128) return launch_d<128, 128, DENSE, OutT>(a, stream);
+  if (a.blk_q == 64 && a.blk_k == 64) return launch_d<64, 64, DENSE, OutT>(a, stream);
+  if (a.blk_q == 128 && a.blk_k == 64) return launch_d<128, 64, DENSE, OutT>(a, stream);
+  if (a.blk_q == 64 && a.blk_k == 128) return launch_d<64, 128, DENSE, OutT>(a, stream);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t stream) {
-  return launch_any<false>(a, stream);
+  return a.out_f32 ? launch_any<false, float>(a, stream) : launch_any<false, __bf16>(a, stream);
 }
 
 hipError_t launch_attention_dense(const AttnArgs& a, hipStream_t stream) {
-  return launch_any<true>(a, stream);
+  if (a.out_f32) return hipErrorInvalidValue;  // the maskless path writes bf16 only
+  return launch_any<true, __bf16>(a, stream);
 }
 
 }  // namespace sa

@@ -24,6 +24,7 @@ struct AttnArgs {
   // element strides of q, k, v and out: batch, head, token (the head-dim is contiguous)
   int64_t sb, sh;
   int sn;
+  bool out_f32 = false;  // out is fp32 instead of bf16 (masked path only)
 };
 
 hipError_t launch_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb, int32_t* counts,

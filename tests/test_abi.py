@@ -96,6 +96,26 @@ def test_other_entry_points_reject_bad_arguments(lib):
     assert lib.sa_bsattn_plan_destroy(None) == binding.SA_ERR_INVALID_ARG
 
 
+def test_f32out_entry_points_reject_bad_arguments_on_host(lib):
+    P = ctypes.c_void_p
+
+    def call(q=A, out=A + 4 * MB, lse=A + 5 * MB, d=128):
+        return lib.sa_bsattn_fwd_f32out(P(q), P(A + MB), P(A + 2 * MB), P(A + 3 * MB), P(out),
+                                        P(lse), 1, 2, 256, d, 128, 128, ctypes.c_float(0.088),
+                                        None)
+    # every call carries at least one invalid argument
+    out_bf16_bytes = 2 * 256 * 128 * 2
+    assert call(q=0) == binding.SA_ERR_INVALID_ARG
+    assert call(out=A + 4 * MB + 8) == binding.SA_ERR_INVALID_ARG          # misaligned out
+    assert call(d=96) == binding.SA_ERR_UNSUPPORTED
+    # lse just past a bf16 out of this shape: inside the float32 out, so rejected
+    assert call(lse=A + 4 * MB + out_bf16_bytes) == binding.SA_ERR_INVALID_ARG
+    # an fp32 out starting half its size before v overlaps v
+    assert call(out=A + 2 * MB - out_bf16_bytes) == binding.SA_ERR_INVALID_ARG
+    assert lib.sa_bsattn_fwd_plan_f32out(None, P(A), P(A), P(A), P(A), P(A), 128,
+                                         ctypes.c_float(1.0), None) == binding.SA_ERR_INVALID_ARG
+
+
 def _dense(lib, q=A, k=A + MB, v=A + 2 * MB, out=A + 4 * MB, lse=A + 5 * MB,
            B=1, H=2, N=256, d=128, blk=128, scale=0.088):
     P = ctypes.c_void_p

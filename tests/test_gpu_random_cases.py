@@ -9,14 +9,16 @@ two-item ping-pong kernel for 128-row items, the one-item kernel for 64-row
 items) together with the schedule's window sort at small n_qb.  Input scales
 reach 2, where rows are nearly one-hot and |out| reaches 4-8: the out bound
 per element takes the bf16 rounding of P into account (helpers.compare,
-pv_abs).
+pv_abs).  The float32-out entry points run on the same inputs: their out meets
+the plain 2e-2 bound with no allowance for rounding out, and rounds to the
+bf16 out bit for bit.
 """
 
 import numpy as np
 import pytest
 
 import oracle
-from helpers import compare, to_bits
+from helpers import BF16_UNIT_ROUNDOFF, OUT_MAX_ABS, OUT_MEAN_ABS, compare, to_bits
 from workloads import pack_rows
 
 pytestmark = pytest.mark.gpu
@@ -80,12 +82,26 @@ def test_random_case(seed):
         out, lse = binding.bsattn_fwd(q, k, v, packed, c["blk_q"], c["blk_k"], scale)
     torch.cuda.synchronize()
     compare(out.float().cpu().numpy(), lse.cpu().numpy(), ref_out, ref_lse, pv_abs=pv_abs)
+    # float32 out: the strict bounds with no allowance for rounding out, and the bf16 out is
+    # its round-to-nearest-even (same arithmetic up to the last step)
+    out32, lse32 = binding.bsattn_fwd_f32out(q, k, v, packed, c["blk_q"], c["blk_k"], scale)
+    torch.cuda.synchronize()
+    err32 = np.abs(out32.cpu().numpy().astype(np.float64) - ref_out)
+    bound = BF16_UNIT_ROUNDOFF * pv_abs + 1e-3
+    worst = np.unravel_index(np.argmax(err32 - bound), err32.shape)
+    assert err32.max() <= OUT_MAX_ABS and err32.mean() <= OUT_MEAN_ABS, (err32.max(), err32.mean())
+    assert np.all(err32 <= bound), ("float32 out", worst, err32[worst], bound[worst])
+    out_bhnd = out if c["layout"] == "bhnd" else out.contiguous()
+    assert torch.equal(out32.to(torch.bfloat16), out_bhnd)
+    assert torch.equal(lse32, lse)
     if c["layout"] == "bhnd":
         plan = binding.Plan(packed, c["B"], c["H"], c["N"], c["blk_q"], c["blk_k"])
         try:
             assert plan.executed_blocks == c["B"] * int(bm.sum())
             out_p, lse_p = plan(q, k, v, scale)
+            out32_p, lse32_p = plan.fwd_f32out(q, k, v, scale)
             torch.cuda.synchronize()
             assert torch.equal(out_p, out) and torch.equal(lse_p, lse)
+            assert torch.equal(out32_p, out32) and torch.equal(lse32_p, lse32)
         finally:
             plan.close()
