@@ -242,6 +242,11 @@ def test_binding_rejects_mismatched_sizes_before_any_device_call():
         binding.bsattn_fwd(q, q, q, good_mask, 128, 128,
                            lse=torch.zeros((1, 2, 255)))                              # lse shape
     with pytest.raises(ValueError):
+        binding.bsattn_fwd_f32out(q, q, q, np.zeros((2, 1, 1), dtype=np.uint64), 128, 128)
+    with pytest.raises(ValueError):
+        binding.bsattn_fwd_f32out(q, q, q, good_mask, 128, 128,
+                                  out=torch.zeros((1, 2, 255, 64)))                   # out shape
+    with pytest.raises(ValueError):
         binding.bsattn_fwd_bnhd(q, q, q, np.zeros((256, 2, 1), dtype=np.uint64), 128, 128)
     with pytest.raises(ValueError):
         binding.dense_attn_fwd(q, q, q[..., :32])
