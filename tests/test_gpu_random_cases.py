@@ -1,6 +1,6 @@
 """Seeded random shapes through the C ABI against the float64 reference.
 
-Each case draws B, H, N (ragged tails included), d, blk_q and blk_k
+Each of 64 cases draws B, H, N (ragged tails included), d, blk_q and blk_k
 independently, a density (empty rows and an all-empty head included), a
 per-case input scale, and the tensor layout, then checks the one-shot call
 and the static-mask plan: both against the reference, and the plan bit for bit
@@ -23,7 +23,7 @@ from workloads import pack_rows
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 24
+N_CASES = 64
 
 
 def _case(seed):
