@@ -15,7 +15,7 @@
 
 namespace {
 
-constexpr int kVersion = 100;  // 0.1.0
+constexpr int kVersion = 200;  // 0.2.0: float32-out entry points
 
 struct Dims {
   int n_qb, n_kb, W;
