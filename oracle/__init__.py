@@ -43,5 +43,4 @@ from .attention import (  # noqa: F401
     attention_block,
     attention,
     attention_sampled,
-    attention_probs_block,
 )

@@ -46,30 +46,6 @@ def _allowed_keys(allowed_kb, blk_k, n_tokens):
     return allowed_kb[j // blk_k]
 
 
-def attention_probs_block(q_rows, k, allowed_kb, blk_k, scale):
-    """Attention probabilities P[i, j] of some query rows of one block.
-
-    ``q_rows`` [nq, d]; ``k`` [N, d]; ``allowed_kb`` bool [n_kb].  Returns
-    (P [nq, N], lse [nq]); P is zero outside the allowed keys.
-    """
-    q_rows = _as_f64(q_rows)
-    k = _as_f64(k)
-    n_tokens = k.shape[0]
-    keys = _allowed_keys(allowed_kb, blk_k, n_tokens)
-    nq = q_rows.shape[0]
-    P = np.zeros((nq, n_tokens), dtype=np.float64)
-    lse = np.full(nq, -np.inf, dtype=np.float64)
-    if nq == 0 or not keys.any():
-        return P, lse
-    s = scale * (q_rows @ k[keys].T)
-    m = s.max(axis=1, keepdims=True)
-    e = np.exp(s - m)
-    l = e.sum(axis=1, keepdims=True)
-    lse[:] = (m + np.log(l))[:, 0]
-    P[:, keys] = np.exp(s - lse[:, None])
-    return P, lse
-
-
 def attention_block(q_rows, k, v, allowed_kb, blk_k, scale):
     """Output and lse of some query rows that share one CRM row.
 

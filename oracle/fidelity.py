@@ -67,11 +67,6 @@ def dense_row(q_row, k, scale):
     return _softmax_over(logits(q_row, k, scale))
 
 
-def sparse_row(q_row, k, allowed_keys, scale):
-    """Softmax restricted to the allowed keys, zero elsewhere; None if nothing is allowed."""
-    return _softmax_over(logits(q_row, k, scale), allowed_keys)
-
-
 def profile(q, k, rows, T, p_cands, blk, scale):
     """Fidelity profile of threshold-map masks on sampled rows.
 

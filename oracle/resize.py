@@ -15,7 +15,8 @@ one).  Readings:
 
 * For a 0/1 mask, ceil(Phi) is 1 exactly when some base block with a
   positive interpolation weight is 1: the resize keeps every block that any
-  neighbour keeps ("any overlap with active regions is preserved").
+  neighbour keeps, which is the conservative property Eq. 7 is meant to have
+  (no active region of the base map is lost at the target resolution).
 * The paper resizes the threshold map.  A ceiling of interpolated thresholds
   would send every value in (0, 1] to 1, so the reading taken is the operator
   that commutes with instantiation: T_target(u, v) is the minimum of T_base

@@ -143,6 +143,19 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _used_on(stream, *tensors):
+    """Tensors made here and used by work on a stream other than the current one:
+    the caching allocator must not hand their memory out again before that
+    stream's work on them is done (it only tracks the current stream by itself)."""
+    if stream is None:
+        return
+    torch = _torch()
+    if stream == torch.cuda.current_stream():
+        return
+    for t in tensors:
+        t.record_stream(stream)
+
+
 def mask_to_device(mask_bits, device="cuda"):
     """uint64 numpy [H, n_qb, W] -> int64 torch tensor (same bits) on ``device``."""
     torch = _torch()
@@ -170,6 +183,7 @@ def _fwd_oneshot(fn, out_dtype, q, k, v, mask_bits, blk_q, blk_k, scale, out, ls
         _dev_ptr(out, out_dtype, "out"), _dev_ptr(lse, torch.float32, "lse"),
         B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
     _check(fn, st)
+    _used_on(stream, m, out, lse)
     return out, lse
 
 
@@ -210,6 +224,7 @@ def bsattn_fwd_bnhd(q, k, v, mask_bits, blk_q, blk_k, scale=None, out=None, lse=
         _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
         B, H, N, d, int(blk_q), int(blk_k), float(scale), SA_LAYOUT_BNHD, _stream(stream))
     _check("sa_bsattn_fwd_layout", st)
+    _used_on(stream, m, out, lse)
     return out, lse
 
 
@@ -227,6 +242,7 @@ def dense_attn_fwd(q, k, v, blk=128, scale=None, out=None, lse=None, stream=None
         _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, torch.bfloat16, "out"),
         _dev_ptr(lse, torch.float32, "lse"), B, H, N, d, int(blk), float(scale), _stream(stream))
     _check("sa_dense_attn_fwd", st)
+    _used_on(stream, out, lse)
     return out, lse
 
 
@@ -250,6 +266,7 @@ def mask_instantiate(T, p, out=None, stream=None):
                                  n_p, H, n_qb, n_kb, _dev_ptr(out, torch.int64, "mask_bits"),
                                  _stream(stream))
     _check("sa_mask_instantiate", st)
+    _used_on(stream, out)
     return out
 
 
@@ -281,6 +298,7 @@ def fidelity_profile(q, k, rows, T, p, blk, scale=None, stream=None):
         _dev_ptr(hel, torch.float32, "hellinger"), _dev_ptr(fid, torch.float32, "fidelity"),
         B, H, N, d, int(blk), float(scale), _stream(stream))
     _check("sa_fidelity_profile", st)
+    _used_on(stream, blk_lse, hel, fid)
     return hel, fid, blk_lse
 
 
@@ -294,6 +312,7 @@ def resize_threshold_map(T, n_qb_out, n_kb_out, stream=None):
                                      _dev_ptr(out, torch.float32, "T_out"), n_qb_out, n_kb_out,
                                      _stream(stream))
     _check("sa_resize_threshold_map", st)
+    _used_on(stream, out)
     return out
 
 
@@ -311,6 +330,7 @@ def resize_mask(mask_bits, n_kb, n_qb_out, n_kb_out, stream=None):
                             _dev_ptr(out, torch.int64, "mask_out"), n_qb_out, n_kb_out,
                             _stream(stream))
     _check("sa_resize_mask", st)
+    _used_on(stream, m, out)
     return out
 
 
@@ -328,6 +348,7 @@ def mask_prepass(mask_bits, H, n_qb, n_kb, stream=None):
                              _dev_ptr(counts, torch.int32, "counts"),
                              _dev_ptr(lists, torch.int32, "lists"), _stream(stream))
     _check("sa_mask_prepass", st)
+    _used_on(stream, m, counts, lists)
     return counts, lists
 
 
@@ -340,6 +361,7 @@ def schedule(counts, B, H, n_qb, stream=None):
     st = lib.sa_schedule(_dev_ptr(counts, torch.int32, "counts"), B, H, n_qb,
                          _dev_ptr(order, torch.int32, "order"), _stream(stream))
     _check("sa_schedule", st)
+    _used_on(stream, order)
     return order
 
 
@@ -364,6 +386,7 @@ def bsattn_fwd_prepared(q, k, v, counts, lists, order, blk_q, blk_k, scale=None,
         _dev_ptr(out, torch.bfloat16, "out"), _dev_ptr(lse, torch.float32, "lse"),
         B, H, N, d, int(blk_q), int(blk_k), float(scale), _stream(stream))
     _check("sa_bsattn_fwd_prepared", st)
+    _used_on(stream, out, lse)
     return out, lse
 
 
@@ -404,6 +427,7 @@ class Plan:
             _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(out, out_dtype, "out"),
             _dev_ptr(lse, torch.float32, "lse"), d, float(scale), _stream(stream))
         _check(fn, st)
+        _used_on(stream, out, lse)
         return out, lse
 
     def __call__(self, q, k, v, scale=None, out=None, lse=None, stream=None):

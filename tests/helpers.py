@@ -66,6 +66,39 @@ def compare(out_gpu, lse_gpu, out_ref, lse_ref, pv_abs=None):
     return stats
 
 
+def compare_strict(out_gpu, lse_gpu, out_ref, lse_ref):
+    """The plain bounds with no allowance for rounding the output: out max-abs
+    <= OUT_MAX_ABS and mean-abs <= OUT_MEAN_ABS over every checked element,
+    lse max-abs <= LSE_MAX_ABS over the finite ones.  For float32 outputs."""
+    out_gpu = np.asarray(out_gpu, dtype=np.float64)
+    out_ref = np.asarray(out_ref, dtype=np.float64)
+    lse_gpu = np.asarray(lse_gpu, dtype=np.float64)
+    lse_ref = np.asarray(lse_ref, dtype=np.float64)
+    assert out_gpu.shape == out_ref.shape and lse_gpu.shape == lse_ref.shape
+    assert np.all(np.isfinite(out_gpu)), "non-finite output"
+    fin_ref = np.isfinite(lse_ref)
+    assert np.array_equal(np.isfinite(lse_gpu), fin_ref), "lse finiteness differs"
+    err = np.abs(out_gpu - out_ref)
+    lse_err = np.abs(lse_gpu[fin_ref] - lse_ref[fin_ref])
+    stats = dict(out_max_abs=float(err.max()) if err.size else 0.0,
+                 out_mean_abs=float(err.mean()) if err.size else 0.0,
+                 lse_max_abs=float(lse_err.max()) if lse_err.size else 0.0)
+    assert stats["out_max_abs"] <= OUT_MAX_ABS, stats
+    assert stats["out_mean_abs"] <= OUT_MEAN_ABS, stats
+    assert stats["lse_max_abs"] <= LSE_MAX_ABS, stats
+    return stats
+
+
+def gather_rows(t, items, blk_q, N):
+    """Rows of the (b, h, u) query blocks of a [B, H, N, ...] device tensor, on the host,
+    concatenated in item order."""
+    parts = []
+    for (b, h, u) in items:
+        r0, r1 = u * blk_q, min((u + 1) * blk_q, N)
+        parts.append(t[b, h, r0:r1].float().cpu().numpy())
+    return np.concatenate(parts)
+
+
 def to_bits(t):
     """bf16 torch tensor -> host uint16 bit array."""
     import torch

@@ -212,16 +212,6 @@ def test_sampled_matches_full():
         assert np.array_equal(o, out[b, h, sl]) and np.array_equal(l, lse[b, h, sl])
 
 
-def test_probs_rows_sum_to_one_and_vanish_outside():
-    N, d, blk = 80, 6, 16
-    q = _rand((16, d), 40, -3, 3)
-    k = _rand((N, d), 41, -3, 3)
-    allowed = np.array([True, False, False, True, True])
-    P, lse = oracle.attention_probs_block(q, k, allowed, blk, 0.9)
-    assert np.allclose(P.sum(axis=1), 1.0, atol=1e-14)
-    assert np.all(P[:, 16:48] == 0.0)
-
-
 # ---------------------------------------------------------- bit-level pins ---
 
 def test_bf16_decode_known_patterns():
