@@ -55,6 +55,7 @@ extern "C" {
 #define SA_ERR_INVALID_ARG 1 /* null/misaligned pointer, bad size, bad scale, aliasing */
 #define SA_ERR_UNSUPPORTED 2 /* shape outside the supported set above */
 #define SA_ERR_HIP 3         /* a HIP allocation or launch failed */
+#define SA_ERR_TOO_LARGE 4   /* workspace beyond SA_NOALLOC_SCRATCH_BYTES (sa_bsattn_fwd_noalloc) */
 
 /* Human-readable text for a status code (static storage, never NULL). */
 SA_API const char* sa_status_string(int status);
@@ -73,6 +74,31 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v,
                          const uint64_t* mask_bits, void* out, float* lse,
                          int B, int H, int N, int d, int blk_q, int blk_k,
                          float scale, void* stream);
+
+/*
+ * One-shot forward pass as sa_bsattn_fwd that allocates nothing, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  The workspace of the
+ * pre-pass and the schedule (counts, lists and order: 4 H n_qb +
+ * 4 H n_qb n_kb + 4 B H n_qb bytes, each part rounded up to 256) lives in a
+ * fixed array of SA_NOALLOC_SCRATCH_BYTES in the library's device memory,
+ * one per GPU, held from the library's load onto that GPU until the process
+ * ends.  A larger workspace returns SA_ERR_TOO_LARGE before anything is
+ * enqueued (14B-like 720p, H 40 and 591 x 591 blocks, needs 56 MB).
+ * The first call on a device looks the array's address up there
+ * (hipGetSymbolAddress).  Every call on one GPU shares that GPU's array:
+ * calls whose work overlaps in time on one GPU (other streams, other host
+ * threads) race on it and give wrong results, so order them (one stream, or
+ * events).  Nothing in the array needs to start at zero: each call writes
+ * every entry it reads.  Arguments, layout, results and the other errors as
+ * sa_bsattn_fwd; the result is bit for bit that of sa_bsattn_fwd.
+ */
+#define SA_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+SA_API int sa_bsattn_fwd_noalloc(const void* q, const void* k, const void* v,
+                                 const uint64_t* mask_bits, void* out, float* lse,
+                                 int B, int H, int N, int d, int blk_q, int blk_k,
+                                 float scale, void* stream);
 
 /*
  * One-shot forward pass as sa_bsattn_fwd, with out in float32 (contiguous

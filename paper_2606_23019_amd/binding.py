@@ -16,6 +16,7 @@ SA_OK = 0
 SA_ERR_INVALID_ARG = 1
 SA_ERR_UNSUPPORTED = 2
 SA_ERR_HIP = 3
+SA_ERR_TOO_LARGE = 4
 SA_LAYOUT_BHND = 0
 SA_LAYOUT_BNHD = 1
 
@@ -36,6 +37,7 @@ SIGNATURES = {
     "sa_bsattn_plan_create": (_I, [_P, _I, _I, _I, _I, _I, _P, ctypes.POINTER(_P)]),
     "sa_bsattn_fwd_plan": (_I, [_P, _P, _P, _P, _P, _P, _I, _F, _P]),
     "sa_bsattn_fwd_f32out": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
+    "sa_bsattn_fwd_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
     "sa_bsattn_fwd_plan_f32out": (_I, [_P, _P, _P, _P, _P, _P, _I, _F, _P]),
     "sa_bsattn_plan_stats": (_I, [_P, ctypes.POINTER(ctypes.c_int64)]),
     "sa_bsattn_plan_destroy": (_I, [_P]),

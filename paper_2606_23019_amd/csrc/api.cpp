@@ -8,6 +8,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 
 #include "../../include/sa_bsattn.h"
@@ -15,7 +16,7 @@
 
 namespace {
 
-constexpr int kVersion = 200;  // 0.2.0: float32-out entry points
+constexpr int kVersion = 300;  // 0.3.0: allocation-free one-shot entry point
 
 struct Dims {
   int n_qb, n_kb, W;
@@ -103,6 +104,7 @@ SA_API const char* sa_status_string(int status) {
     case SA_ERR_INVALID_ARG: return "invalid argument";
     case SA_ERR_UNSUPPORTED: return "unsupported shape";
     case SA_ERR_HIP: return "HIP runtime error";
+    case SA_ERR_TOO_LARGE: return "workspace larger than the fixed scratch of the allocation-free entry point";
     default: return "unknown status";
   }
 }
@@ -208,32 +210,37 @@ SA_API int sa_bsattn_fwd_prepared(const void* q, const void* k, const void* v,
                       false, stream);
 }
 
-// One-shot forward for either tensor layout (strides in elements); out is
-// bf16 or, with out_f32, fp32.
-static int fwd_oneshot(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
-                       void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
-                       float scale, int layout, bool out_f32, void* stream) {
-  Dims dm;
-  int st = check_shape(B, H, N, blk_q, blk_k, &dm);
+// Checks of a one-shot call (either tensor layout; out bf16 or, with out_f32,
+// fp32), before anything is enqueued.
+static int check_oneshot(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
+                         const void* out, const float* lse, int B, int H, int N, int d, int blk_q,
+                         int blk_k, float scale, int layout, bool out_f32, Dims* dm) {
+  int st = check_shape(B, H, N, blk_q, blk_k, dm);
   if (st != SA_OK) return st;
   if (!mask_bits || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
   if (layout != SA_LAYOUT_BHND && layout != SA_LAYOUT_BNHD) return SA_ERR_INVALID_ARG;
-  st = check_tensors(q, k, v, mask_bits, (size_t)H * dm.n_qb * dm.W, out, lse, B, H, N, d, scale,
+  st = check_tensors(q, k, v, mask_bits, (size_t)H * dm->n_qb * dm->W, out, lse, B, H, N, d, scale,
                      out_f32 ? 4 : 2);
   if (st != SA_OK) return st;
-  const bool bnhd = layout == SA_LAYOUT_BNHD;
-  const int sn = bnhd ? H * d : d;
+  const int sn = layout == SA_LAYOUT_BNHD ? H * d : d;
   // tile copies address a tile with 32-bit byte offsets
   if ((int64_t)sn * (blk_k > blk_q ? blk_k : blk_q) * 2 >= ((int64_t)1 << 31)) return SA_ERR_UNSUPPORTED;
+  return SA_OK;
+}
 
-  hipStream_t s = (hipStream_t)stream;
+// Pre-pass, schedule and attention of a checked one-shot call, with the
+// workspace laid out by plan_workspace at ws.
+static hipError_t launch_oneshot(const void* q, const void* k, const void* v,
+                                 const uint64_t* mask_bits, void* out, float* lse, int B, int H,
+                                 int N, int d, int blk_q, int blk_k, float scale, int layout,
+                                 bool out_f32, const Dims& dm, void* ws, hipStream_t s) {
   const Workspace w = plan_workspace(B, H, dm);
-  void* ws = nullptr;
-  if (hipMallocAsync(&ws, w.total, s) != hipSuccess || !ws) return SA_ERR_HIP;
   char* base = (char*)ws;
   int32_t* counts = (int32_t*)(base + w.counts_off);
   int32_t* lists = (int32_t*)(base + w.lists_off);
   int32_t* order = (int32_t*)(base + w.order_off);
+  const bool bnhd = layout == SA_LAYOUT_BNHD;
+  const int sn = bnhd ? H * d : d;
   hipError_t e = sa::launch_prepass(mask_bits, H, dm.n_qb, dm.n_kb, counts, lists, s);
   if (e == hipSuccess) e = sa::launch_schedule(counts, B, H, dm.n_qb, order, s);
   if (e == hipSuccess) {
@@ -243,8 +250,52 @@ static int fwd_oneshot(const void* q, const void* k, const void* v, const uint64
     a.out_f32 = out_f32;
     e = sa::launch_attention(a, s);
   }
+  return e;
+}
+
+// One-shot forward with a stream-ordered workspace.
+static int fwd_oneshot(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
+                       void* out, float* lse, int B, int H, int N, int d, int blk_q, int blk_k,
+                       float scale, int layout, bool out_f32, void* stream) {
+  Dims dm;
+  const int st = check_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale,
+                               layout, out_f32, &dm);
+  if (st != SA_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const Workspace w = plan_workspace(B, H, dm);
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, w.total, s) != hipSuccess || !ws) return SA_ERR_HIP;
+  const hipError_t e = launch_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k,
+                                      scale, layout, out_f32, dm, ws, s);
   const hipError_t ef = hipFreeAsync(ws, s);
   return (e == hipSuccess && ef == hipSuccess) ? SA_OK : SA_ERR_HIP;
+}
+
+// Scratch of the allocation-free entry point: the workspace (counts, lists,
+// order) of one call, in the library's own device memory.  Each GPU holds its
+// copy from the library's load onto it until the process ends.  In host code
+// `scratch` only names the symbol; its device address on the current device
+// comes from hipGetSymbolAddress, looked up once per device and kept below.
+static __device__ __align__(256) unsigned char scratch[SA_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static void* g_scratch_ptr[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the current device (set up on the first call
+// there, with that device current).
+static int scratch_on_current_device(void** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SA_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SA_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SA_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return SA_OK;
 }
 
 SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint64_t* mask_bits,
@@ -252,6 +303,24 @@ SA_API int sa_bsattn_fwd(const void* q, const void* k, const void* v, const uint
                          float scale, void* stream) {
   return fwd_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale,
                      SA_LAYOUT_BHND, false, stream);
+}
+
+SA_API int sa_bsattn_fwd_noalloc(const void* q, const void* k, const void* v,
+                                 const uint64_t* mask_bits, void* out, float* lse, int B, int H,
+                                 int N, int d, int blk_q, int blk_k, float scale, void* stream) {
+  Dims dm;
+  int st = check_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k, scale,
+                         SA_LAYOUT_BHND, false, &dm);
+  if (st != SA_OK) return st;
+  if (plan_workspace(B, H, dm).total > (size_t)SA_NOALLOC_SCRATCH_BYTES) return SA_ERR_TOO_LARGE;
+  void* ws = nullptr;
+  st = scratch_on_current_device(&ws);
+  if (st != SA_OK) return st;
+  // Nothing in the scratch has to start at zero: the pre-pass writes every
+  // count and every list entry up to the count, the schedule every order entry.
+  const hipError_t e = launch_oneshot(q, k, v, mask_bits, out, lse, B, H, N, d, blk_q, blk_k,
+                                      scale, SA_LAYOUT_BHND, false, dm, ws, (hipStream_t)stream);
+  return e == hipSuccess ? SA_OK : SA_ERR_HIP;
 }
 
 SA_API int sa_bsattn_fwd_f32out(const void* q, const void* k, const void* v,

@@ -259,3 +259,21 @@ def test_binding_rejects_mismatched_sizes_before_any_device_call():
     with pytest.raises(ValueError):
         binding.fidelity_profile(q, q, torch.zeros((2, 4), dtype=torch.int32),
                                  torch.zeros((2, 3, 2)), torch.zeros(3), 128)         # T shape
+
+
+def test_noalloc_rejects_on_host(lib):
+    """The allocation-free call checks its arguments, then the workspace size
+    against the fixed scratch, before any device work."""
+    P = ctypes.c_void_p
+    f = ctypes.c_float(0.125)
+    args = [P(A), P(A + MB), P(A + 2 * MB), P(A + 3 * MB), P(A + 4 * MB), P(A + 5 * MB)]
+    assert lib.sa_bsattn_fwd_noalloc(P(0), *args[1:], 1, 2, 256, 128, 128, 128, f, None) == \
+        binding.SA_ERR_INVALID_ARG
+    assert lib.sa_bsattn_fwd_noalloc(*args, 1, 2, 256, 96, 128, 128, f, None) == \
+        binding.SA_ERR_UNSUPPORTED
+    # H 70, N 32768, 64 x 64 blocks: 70 * 512 * 512 * 4 bytes of lists alone exceed 64 MiB
+    T = 1 << 33
+    big = [P(A + i * T) for i in range(6)]
+    assert lib.sa_bsattn_fwd_noalloc(*big, 1, 70, 32768, 64, 64, 64, f, None) == \
+        binding.SA_ERR_TOO_LARGE
+    assert "scratch" in binding.status_string(binding.SA_ERR_TOO_LARGE)
