@@ -552,8 +552,12 @@ def main():
                     help="counter-collection run: attention kernel launches plus a plain 1 GiB "
                          "device copy (the HBM byte-counter calibration), nothing else")
     ap.add_argument("--profile-density", type=float, default=None,
-                    help="with --profile: run the structured sweep point of this density "
-                         "(H40 N32768 d128 blk128) instead of the workload")
+                    help="with --profile: run the sweep point of this density (H40 N32768 d128) "
+                         "instead of the workload")
+    ap.add_argument("--profile-blk", type=int, default=128, choices=(64, 128),
+                    help="block size of the --profile-density point")
+    ap.add_argument("--profile-kind", default="structured", choices=("structured", "uniform"),
+                    help="mask kind of the --profile-density point")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -573,7 +577,7 @@ def main():
     wl = SHORT[args.workload]
     if args.profile and args.profile_density is not None:
         from workloads import sweep_point
-        wl = sweep_point(args.profile_density, 128, "structured")
+        wl = sweep_point(args.profile_density, args.profile_blk, args.profile_kind)
     log("workload", wl.name)
     case = Case(wl)
     if args.profile:
