@@ -156,8 +156,8 @@ SA_API int sa_mask_prepass(const uint64_t* mask_bits, int H, int n_qb, int n_kb,
  * output of set i is exactly the mask_bits argument of sa_bsattn_fwd.
  * T: device float32 [H][n_qb][n_kb]; p: device float32 [n_p][H];
  * mask_bits: device uint64 [n_p][H][n_qb][W], W = ceil(n_kb / 64), every word
- * written.  mask_bits must not overlap T or p.  Requires n_p, H, n_qb >= 1
- * and 1 <= n_kb <= 65535.
+ * written.  mask_bits must not overlap T or p.  Requires n_p, H, n_qb >= 1,
+ * n_p <= 1048560 and 1 <= n_kb <= 65535.
  */
 SA_API int sa_mask_instantiate(const float* T, const float* p, int n_p, int H, int n_qb, int n_kb,
                                uint64_t* mask_bits, void* stream);

@@ -125,7 +125,7 @@ SA_API int sa_mask_instantiate(const float* T, const float* p, int n_p, int H, i
                                uint64_t* mask_bits, void* stream) {
   if (!T || !p || !mask_bits || n_p < 1 || H < 1 || n_qb < 1 || n_kb < 1) return SA_ERR_INVALID_ARG;
   if (!aligned(T, 4) || !aligned(p, 4) || !aligned(mask_bits, 8)) return SA_ERR_INVALID_ARG;
-  if (n_kb > 65535) return SA_ERR_UNSUPPORTED;
+  if (n_kb > 65535 || n_p > 16 * 65535) return SA_ERR_UNSUPPORTED;
   const int64_t rows = (int64_t)H * n_qb;
   const int64_t W = (n_kb + 63) / 64;
   if (rows >= ((int64_t)1 << 31) || (int64_t)n_p * rows * W >= ((int64_t)1 << 40))

@@ -2,14 +2,16 @@
 // density threshold p is M_p = 1[T <= p], one comparison per block, stored in
 // the CRM layout (LSB-first uint64 words per query-block row).
 //
-// One wavefront per row (h, u), eight words at a time.  Lane l loads
-// T[h][u][64 w + l] for the eight words of the group into registers (all loads
-// in flight together); then for every threshold p[i][h] a wavefront ballot of
-// the comparison is the word itself (ballot bit l is lane l's predicate, i.e.
-// key block 64 w + l at bit l), lane k keeps word k, and the
-// group's words leave in one 64-byte store.  The map is read from memory once
-// for all thresholds (a head's map serves every timestep of its layer): 4 bytes
-// read per block, one bit written per block and threshold, three vector
+// One wavefront per row (h, u) and set of up to 16 thresholds, eight words at
+// a time.  Lane l loads T[h][u][64 w + l] for the eight words of the group
+// into registers (all loads in flight together); then for every threshold
+// p[i][h] a wavefront ballot of the comparison is the word itself (ballot bit
+// l is lane l's predicate, i.e. key block 64 w + l at bit l), lane k keeps
+// word k, and the group's words leave in one 64-byte store.  The thresholds of
+// a wavefront come in with one vector load, so no scalar load waits inside the
+// threshold loop.  The map is read from memory once per 16 thresholds (a
+// head's map serves every timestep of its layer; the re-reads hit in L2): 4
+// bytes read per block, one bit written per block and threshold, three vector
 // instructions per 64 bits.
 
 #include "device_common.h"
@@ -20,7 +22,8 @@ namespace sa {
 namespace {
 
 constexpr int kInstWaves = 4;
-constexpr int kGroup = 8;  // words whose map entries a lane holds in registers at once
+constexpr int kGroup = 8;     // words whose map entries a lane holds in registers at once
+constexpr int kInstThr = 16;  // thresholds per wavefront (grid.y splits larger sets)
 
 __global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
     const float* __restrict__ T, const float* __restrict__ p, int n_p, int H, int n_qb, int n_kb,
@@ -30,6 +33,11 @@ __global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
   const int64_t row = (int64_t)blockIdx.x * kInstWaves + (threadIdx.x >> 6);
   if (row >= rows) return;  // uniform per wavefront
   const int h = (int)(row / n_qb);
+  const int i_first = blockIdx.y * kInstThr;
+  const int n_thr = min(kInstThr, n_p - i_first);
+  // this wavefront's thresholds, lane k holding p[i_first + k][h], read once
+  // with one vector load and handed to the comparisons by readlane
+  const float p_lane = lane < n_thr ? p[(int64_t)(i_first + lane) * H + h] : 0.f;
   const float* trow = T + row * n_kb;
   for (int w0 = 0; w0 < W; w0 += kGroup) {
     const int nw = min(kGroup, W - w0);
@@ -40,8 +48,10 @@ __global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
       const int v = (w0 + k) * 64 + lane;
       t[k] = (k < nw && v < n_kb) ? trow[v] : __builtin_nanf("");  // NaN: never on
     }
-    for (int i = 0; i < n_p; ++i) {
-      const float pi = p[(int64_t)i * H + h];
+#pragma unroll
+    for (int i = 0; i < kInstThr; ++i) {
+      if (i >= n_thr) break;  // uniform
+      const float pi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p_lane), i));
       uint32_t lo = 0, hi = 0;  // lane k ends up holding word w0 + k
 #pragma unroll
       for (int k = 0; k < kGroup; ++k) {
@@ -53,7 +63,9 @@ __global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
           }
         }
       }
-      if (lane < nw) bits[((int64_t)i * rows + row) * W + w0 + lane] = ((uint64_t)hi << 32) | lo;
+      if (lane < nw)
+        bits[((int64_t)(i_first + i) * rows + row) * W + w0 + lane] =
+            ((uint64_t)hi << 32) | lo;
     }
   }
 }
@@ -65,8 +77,10 @@ hipError_t launch_mask_instantiate(const float* T, const float* p, int n_p, int 
   const int64_t rows = (int64_t)H * n_qb;
   const int W = (n_kb + 63) / 64;
   const int64_t grid = (rows + kInstWaves - 1) / kInstWaves;
-  hipLaunchKernelGGL(mask_inst_kernel, dim3((unsigned)grid), dim3(64 * kInstWaves), 0, stream, T, p,
-                     n_p, H, n_qb, n_kb, W, bits);
+  const int chunks = (n_p + kInstThr - 1) / kInstThr;
+  if (chunks > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(mask_inst_kernel, dim3((unsigned)grid, (unsigned)chunks), dim3(64 * kInstWaves),
+                     0, stream, T, p, n_p, H, n_qb, n_kb, W, bits);
   return hipGetLastError();
 }
 

@@ -39,6 +39,9 @@ SHAPES = [
     (2, 4, 591, 5, 6),
     (1, 2, 4097, 2, 7),     # 65 words: two chunks of the row loop
     (2, 2, 65535, 1, 8),    # largest supported row
+    (3, 6, 256, 16, 9),     # one full set of 16 thresholds per wavefront
+    (2, 5, 300, 17, 10),    # 16 + 1: a second set of one threshold
+    (4, 9, 591, 50, 11),    # the 50 timesteps of one layer: 4 sets, the last of 2
 ]
 
 

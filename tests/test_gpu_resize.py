@@ -25,6 +25,10 @@ SIZES = [
     (2, 13, 17, 13, 17, 5),      # equal size
     (2, 40, 70, 100, 130, 6),    # crosses word boundaries
     (40, WAN14B_480P.n_qb, WAN14B_480P.n_kb, WAN14B_720P.n_qb, WAN14B_720P.n_kb, 7),  # 480p -> 720p
+    (1, 2, 3000, 3, 8192, 8),    # mask: widest target with the column table in LDS
+    (1, 3, 100, 4, 9000, 9),     # mask: target too wide for the table (points computed per word)
+    (2, 5, 4100, 7, 5000, 10),   # base rows of 65 words, target rows of 79
+    (3, 9, 11, 17, 13, 11),      # 17 target rows: a workgroup's last wavefront has fewer rows
 ]
 
 
