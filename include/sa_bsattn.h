@@ -265,7 +265,12 @@ SA_API int sa_fidelity_profile(const void* q, const void* k, const int32_t* rows
                                int blk, float scale, void* stream);
 
 /*
- * Plan API for static masks.  sa_bsattn_plan_create allocates the plan's
+ * Plan API for static masks (the paper's masks are built offline and reused
+ * for every prompt: Sec. 4 overview figure, "Reuse for All Prompts"; the
+ * executed blocks are those of Sec. 4.3.2's CRM rows).  A plan holds the
+ * result of the CRM walk (the pre-pass) and the work schedule for one mask,
+ * so that each forward pass runs only the attention kernel.
+ * sa_bsattn_plan_create allocates the plan's
  * device buffers with hipMalloc, runs the pre-pass and schedule on `stream`,
  * then SYNCHRONISES `stream` to record the executed-block count.  The plan
  * keeps no pointer to mask_bits.  A plan is bound to the device that was
@@ -279,7 +284,8 @@ SA_API int sa_bsattn_plan_create(const uint64_t* mask_bits, int B, int H, int N,
                                  int blk_q, int blk_k, void* stream, sa_plan_t* plan);
 
 /*
- * Attention with a plan (on the device that was current at creation, else
+ * Attention with a plan (Sec. 4.3.2, on the plan's precomputed block lists;
+ * on the device that was current at creation, else
  * SA_ERR_INVALID_ARG): only the attention kernel is enqueued (no
  * allocation, memset or synchronisation), so the call may be captured into a
  * HIP graph and replayed; the plan and the tensors must outlive the graph.
@@ -291,7 +297,8 @@ SA_API int sa_bsattn_fwd_plan(sa_plan_t plan, const void* q, const void* k, cons
 SA_API int sa_bsattn_fwd_plan_f32out(sa_plan_t plan, const void* q, const void* k, const void* v,
                                      float* out, float* lse, int d, float scale, void* stream);
 
-/* Total executed (b, h, u, v) blocks of the plan: B * sum of all row counts. */
+/* Total executed (b, h, u, v) blocks of the plan: B * sum of all row counts
+ * (the blocks whose CRM bit is set, Sec. 4.3.2). */
 SA_API int sa_bsattn_plan_stats(sa_plan_t plan, int64_t* executed_blocks);
 
 /* Frees the plan (hipFree, which waits for outstanding work on the device). */
