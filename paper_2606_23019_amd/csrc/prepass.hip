@@ -4,9 +4,10 @@
 // kernel with a bit-scan iterator (Sec. 4.3.2 and the appendix "CRM Forward
 // Iterator": skip empty segments, report base + count-trailing-zeros, clear
 // the lowest bit).  Masks are static, so here the walk runs once per row in
-// a separate kernel: one wavefront per row, lane w owns word w, a popcount
-// plus a wavefront prefix sum gives every lane its output offset, and the
-// ctz / clear-lowest loop writes the enabled key blocks in ascending order.
+// a separate kernel: one wavefront per row walks the row's words in order;
+// lane l owns bit l of a word, and the popcount of the word's lower bits is
+// its place after the blocks already written, so the enabled key blocks of a
+// word leave in ascending order in one store.
 // The attention kernel then reads a dense list instead of decoding bits.
 //
 // Schedule: heads have very different densities, so (b, h) groups are
@@ -44,29 +45,29 @@ __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
   if (row >= rows) return;  // uniform per wavefront
   const uint64_t* mrow = mask + (int64_t)row * W;
   int32_t* lrow = lists + (int64_t)row * n_kb;
+  // Word by word: lane l owns bit l of the word (key block 64 w + l); its
+  // place in the list is the number of set bits below it (a popcount of the
+  // masked word), so each word's entries leave in one store, in ascending
+  // order, whatever the number of set bits.
+  const uint64_t below = (1ull << lane) - 1ull;  // bits below this lane's
   int done = 0;  // blocks already written for this row
   for (int w0 = 0; w0 < W; w0 += 64) {
-    const int w = w0 + lane;
-    uint64_t word = 0;
-    if (w < W) {
-      word = mrow[w];
-      const int real = n_kb - w * 64;  // bits of this word that name a real key block
-      if (real < 64) word &= (1ull << real) - 1ull;  // real >= 1 for w < W
+    // 64 words at a time, lane i loading word w0 + i (one round of latency),
+    // then handed to the whole wavefront one by one with readlane
+    uint64_t mine = 0;
+    if (w0 + lane < W) {
+      mine = mrow[w0 + lane];
+      const int real = n_kb - (w0 + lane) * 64;  // bits of this word that name a real key block
+      if (real < 64) mine &= (1ull << real) - 1ull;  // real >= 1 for w < W
     }
-    const int pc = __popcll(word);
-    int incl = pc;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int t = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += t;
+    const int nw = min(64, W - w0);
+    for (int i = 0; i < nw; ++i) {
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)mine, i);
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(mine >> 32), i);
+      const uint64_t word = ((uint64_t)hi << 32) | lo;
+      if ((word >> lane) & 1ull) lrow[done + __popcll(word & below)] = (w0 + i) * 64 + lane;
+      done += __popcll(word);
     }
-    int pos = done + incl - pc;
-    while (word) {
-      const int b = __builtin_ctzll(word);
-      lrow[pos++] = w * 64 + b;
-      word &= word - 1ull;
-    }
-    done += __shfl(incl, 63, 64);
   }
   if (lane == 0) counts[row] = done;
 }
@@ -88,14 +89,26 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
   }
   // Per-head cost: `parts` threads per head each sum a strided share of the
   // head's rows, then add it into LDS (few loads per thread instead of n_qb
-  // dependent-latency loads by one thread).
+  // dependent-latency loads by one thread).  The share's loads go out eight
+  // at a time before any is added, so their latencies overlap instead of
+  // adding up.
   for (int h = tid; h < H; h += kSchedThreads) head_cost[h] = 0;
   __syncthreads();
   const int parts = H < kSchedThreads ? kSchedThreads / H : 1;
   for (int w = tid; w < H * parts; w += kSchedThreads) {
     const int h = w / parts;
+    const int32_t* hrow = counts + (int64_t)h * n_qb;
     uint32_t c = 0;
-    for (int u = w - h * parts; u < n_qb; u += parts) c += (uint32_t)counts[(int64_t)h * n_qb + u];
+    for (int u0 = w - h * parts; u0 < n_qb; u0 += 8 * parts) {
+      int32_t v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int u = u0 + i * parts;
+        v[i] = u < n_qb ? hrow[u] : 0;
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) c += (uint32_t)v[i];
+    }
     atomicAdd(&head_cost[h], c);
   }
   int P = 1;
@@ -125,12 +138,34 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
     }
   }
   // Ascending u inside each chunk here; window_sort_kernel then reorders
-  // each window of a chunk by count.
-  for (int64_t pos = tid; pos < n_items; pos += kSchedThreads) {
-    int u;
-    const int k = xcd_slice(pos, n_units, n_qb, &u);
-    const int unit = (int)(keys[k] & 0xFFFFFFFFu);
-    order[pos] = unit * n_qb + u;
+  // each window of a chunk by count.  A chunk (x, k) is written from its
+  // place, first query block and length, worked out once per chunk: by one
+  // wavefront, its lanes writing the items, when chunks are long, and by
+  // one thread when they are short (fewer than 32 items), so that many
+  // short chunks do not leave most lanes idle.
+  const int q = n_qb / kXcds;
+  const int r = n_qb - q * kXcds;
+  const int n_chunks = kXcds * n_units;
+  if (q + 1 >= 32) {
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    for (int c = wave; c < n_chunks; c += kSchedThreads / 64) {
+      const int x = c % kXcds;
+      const int k = c / kXcds;
+      const int64_t j0 = xcd_prefix(k, x, q, r);
+      const int len = (int)(xcd_prefix(k + 1, x, q, r) - j0);
+      const int item0 = (int)(keys[k] & 0xFFFFFFFFu) * n_qb + xcd_chunk_u0(k, x, q, r);
+      for (int i = lane; i < len; i += 64) order[x + kXcds * (j0 + i)] = item0 + i;
+    }
+  } else {
+    for (int c = tid; c < n_chunks; c += kSchedThreads) {
+      const int x = c % kXcds;
+      const int k = c / kXcds;
+      const int64_t j0 = xcd_prefix(k, x, q, r);
+      const int len = (int)(xcd_prefix(k + 1, x, q, r) - j0);
+      const int item0 = (int)(keys[k] & 0xFFFFFFFFu) * n_qb + xcd_chunk_u0(k, x, q, r);
+      for (int i = 0; i < len; ++i) order[x + kXcds * (j0 + i)] = item0 + i;
+    }
   }
 }
 
