@@ -48,9 +48,7 @@ __global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
       const int v = (w0 + k) * 64 + lane;
       t[k] = (k < nw && v < n_kb) ? trow[v] : __builtin_nanf("");  // NaN: never on
     }
-#pragma unroll
-    for (int i = 0; i < kInstThr; ++i) {
-      if (i >= n_thr) break;  // uniform
+    for (int i = 0; i < n_thr; ++i) {  // uniform trip count
       const float pi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p_lane), i));
       uint32_t lo = 0, hi = 0;  // lane k ends up holding word w0 + k
 #pragma unroll
