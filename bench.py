@@ -664,8 +664,18 @@ def main():
             for _ in range(args.warmup):
                 c.attention_only()
             t, _ = _per_launch_time(c.attention_only, args.steps)
+            # the same kernel on an all-ones mask, same inputs (speedup vs dense)
+            d = Case(w, dense=True, qkv=(c.q, c.k, c.v))
+            for _ in range(2):
+                d.attention_only()
+            td, _ = _per_launch_time(d.attention_only, max(3, args.steps // 4))
+            del d
+            c.attention_only()
+            torch.cuda.synchronize()
             res[name] = dict(workload=w.name, ms=t, tflops=c.flops / (t * 1e-3) / 1e12,
-                             mean_density=float(c.dens.mean()), executed_blocks=c.executed)
+                             mean_density=float(c.dens.mean()), executed_blocks=c.executed,
+                             executed_tflop=c.flops / 1e12, dense_mask_ms=td,
+                             speedup_vs_dense=td / t, parity_spot_check=parity_spot_check(c))
             log(json.dumps(res[name]))
             del c
             torch.cuda.empty_cache()
