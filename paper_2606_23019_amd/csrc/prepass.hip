@@ -22,9 +22,9 @@
 // time, on neighbouring query blocks that share most key blocks in
 // structured masks, so their K/V tiles are reused from its L2, and every XCD
 // gets an equal slice of every group, so the load stays balanced.  One
-// workgroup computes each group's total enabled blocks, sorts the groups
-// with a bitonic network in LDS and writes the order, each chunk in
-// ascending u; a second kernel then sorts every window of up to 64 places of
+// workgroup computes each group's total enabled blocks, ranks the groups in
+// LDS (by counting smaller keys, or with a bitonic network beyond 512 groups)
+// and writes the order, each chunk in ascending u; a second kernel then sorts every window of up to 64 places of
 // a chunk by enabled-block count, so that the items the attention kernel
 // runs side by side have similar counts.
 
@@ -73,6 +73,7 @@ __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
 }
 
 constexpr int kSchedThreads = 1024;
+constexpr int kRankSortMax = 512;  // groups ranked by counting; more use the bitonic network
 constexpr int kSchedWindow = 64;  // one wavefront
 
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ counts,
@@ -80,6 +81,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
                                                                   int32_t* __restrict__ order) {
   __shared__ uint64_t keys[kScheduleMaxUnits];
   __shared__ uint32_t head_cost[kScheduleMaxUnits];
+  __shared__ uint32_t rank_unit[kScheduleMaxUnits];  // group index by rank
   const int tid = threadIdx.x;
   const int n_units = B * H;
   const int64_t n_items = (int64_t)n_units * n_qb;
@@ -111,60 +113,71 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
     }
     atomicAdd(&head_cost[h], c);
   }
-  int P = 1;
-  while (P < n_units) P <<= 1;
   __syncthreads();
-  // Ascending sort of (~cost, index): decreasing cost, ties by increasing index.
-  for (int i = tid; i < P; i += kSchedThreads) {
-    keys[i] = (i < n_units)
-                  ? ((uint64_t)(0xFFFFFFFFu - head_cost[i % H]) << 32) | (uint32_t)i
-                  : ~0ull;
-  }
-  __syncthreads();
-  for (int k = 2; k <= P; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < P; i += kSchedThreads) {
-        const int p = i ^ j;
-        if (p > i) {
-          const uint64_t a = keys[i], b = keys[p];
-          const bool up = (i & k) == 0;
-          if ((a > b) == up) {
-            keys[i] = b;
-            keys[p] = a;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  }
-  // Ascending u inside each chunk here; window_sort_kernel then reorders
-  // each window of a chunk by count.  A chunk (x, k) is written from its
-  // place, first query block and length, worked out once per chunk: by one
-  // wavefront, its lanes writing the items, when chunks are long, and by
-  // one thread when they are short (fewer than 32 items), so that many
-  // short chunks do not leave most lanes idle.
-  const int q = n_qb / kXcds;
-  const int r = n_qb - q * kXcds;
-  const int n_chunks = kXcds * n_units;
-  if (q + 1 >= 32) {
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int lane = tid & 63;
-    for (int c = wave; c < n_chunks; c += kSchedThreads / 64) {
-      const int x = c % kXcds;
-      const int k = c / kXcds;
-      const int64_t j0 = xcd_prefix(k, x, q, r);
-      const int len = (int)(xcd_prefix(k + 1, x, q, r) - j0);
-      const int item0 = (int)(keys[k] & 0xFFFFFFFFu) * n_qb + xcd_chunk_u0(k, x, q, r);
-      for (int i = lane; i < len; i += 64) order[x + kXcds * (j0 + i)] = item0 + i;
+  // Ascending order of the keys (~cost, index): decreasing cost, ties by
+  // increasing index; the keys are distinct.  Up to kRankSortMax groups, each
+  // thread ranks its group by counting the smaller keys (one pass, one
+  // barrier); beyond that a bitonic network over the keys in LDS.
+  if (n_units <= kRankSortMax) {
+    for (int i = tid; i < n_units; i += kSchedThreads)
+      keys[i] = ((uint64_t)(0xFFFFFFFFu - head_cost[i % H]) << 32) | (uint32_t)i;
+    __syncthreads();
+    for (int i = tid; i < n_units; i += kSchedThreads) {
+      const uint64_t mine = keys[i];
+      int rank = 0;
+      for (int o = 0; o < n_units; ++o) rank += keys[o] < mine ? 1 : 0;
+      rank_unit[rank] = (uint32_t)i;
     }
   } else {
-    for (int c = tid; c < n_chunks; c += kSchedThreads) {
-      const int x = c % kXcds;
-      const int k = c / kXcds;
+    int P = 1;
+    while (P < n_units) P <<= 1;
+    for (int i = tid; i < P; i += kSchedThreads) {
+      keys[i] = (i < n_units)
+                    ? ((uint64_t)(0xFFFFFFFFu - head_cost[i % H]) << 32) | (uint32_t)i
+                    : ~0ull;
+    }
+    __syncthreads();
+    for (int k = 2; k <= P; k <<= 1) {
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        for (int i = tid; i < P; i += kSchedThreads) {
+          const int p = i ^ j;
+          if (p > i) {
+            const uint64_t a = keys[i], b = keys[p];
+            const bool up = (i & k) == 0;
+            if ((a > b) == up) {
+              keys[i] = b;
+              keys[p] = a;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+    for (int i = tid; i < n_units; i += kSchedThreads) rank_unit[i] = (uint32_t)(keys[i] & 0xFFFFFFFFu);
+  }
+  __syncthreads();
+  // Ascending u inside each chunk here; window_sort_kernel then reorders
+  // each window of a chunk by count.  One wavefront per group rank k: the
+  // group's 8 chunks interleave into one run of launch positions, from
+  // 8 prefix(k, 7) (prefix is non-increasing in x) to 8 prefix(k + 1, 0) + 7,
+  // so the lanes write consecutive positions, each keeping the positions
+  // whose place j = pos / 8 lies in chunk (pos mod 8, k).  The few positions
+  // at either end that belong to a neighbouring rank are written by that
+  // rank's wavefront.
+  const int q = n_qb / kXcds;
+  const int r = n_qb - q * kXcds;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  for (int k = wave; k < n_units; k += kSchedThreads / 64) {
+    const int64_t p_lo = kXcds * xcd_prefix(k, kXcds - 1, q, r);
+    const int64_t p_hi = min(kXcds * xcd_prefix(k + 1, 0, q, r) + kXcds, n_items);
+    const int base = (int)rank_unit[k] * n_qb;
+    for (int64_t pos = p_lo + lane; pos < p_hi; pos += 64) {
+      const int x = (int)(pos % kXcds);
+      const int64_t j = pos / kXcds;
       const int64_t j0 = xcd_prefix(k, x, q, r);
-      const int len = (int)(xcd_prefix(k + 1, x, q, r) - j0);
-      const int item0 = (int)(keys[k] & 0xFFFFFFFFu) * n_qb + xcd_chunk_u0(k, x, q, r);
-      for (int i = 0; i < len; ++i) order[x + kXcds * (j0 + i)] = item0 + i;
+      if (j >= j0 && j < xcd_prefix(k + 1, x, q, r))
+        order[pos] = base + xcd_chunk_u0(k, x, q, r) + (int)(j - j0);
     }
   }
 }

@@ -141,6 +141,22 @@ def test_schedule_is_an_xcd_sliced_heaviest_first_permutation(n):
                 assert np.all(np.diff(us) == 1)
 
 
+@pytest.mark.parametrize("B,H,n", [(3, 200, 5), (1, 700, 9), (2, 1000, 17)])
+def test_schedule_many_groups_matches_the_documented_order(B, H, n):
+    # more than 512 (b, h) groups: the ranking takes the bitonic network, not the
+    # counting pass; small n_qb gives many ties between heads
+    from paper_2606_23019_amd import binding
+    rng = np.random.default_rng(100 + H)
+    bm = rng.random((H, n, n)) < rng.uniform(0.1, 0.9, size=(H, 1, 1))
+    bm[:, np.arange(n), np.arange(n)] = True
+    counts, _ = binding.mask_prepass(pack_rows(bm), H, n, n)
+    order = binding.schedule(counts, B, H, n).cpu().numpy()
+    cost = bm.reshape(H, -1).sum(axis=1)
+    units = sorted(range(B * H), key=lambda x: (-cost[x % H], x))
+    row_counts = [bm[x % H].sum(axis=1) for x in range(B * H)]
+    assert order.tolist() == _xcd_order(units, n, row_counts)
+
+
 @pytest.mark.parametrize("B,H", [(1, 4097), (2, 2049)])
 def test_schedule_is_the_identity_beyond_4096_groups(B, H):
     # more than 4096 (b, h) groups: no ranking and no window sort, items in index order
