@@ -195,6 +195,57 @@ __device__ __forceinline__ void store_out4(float* p, float a, float b, float c, 
   *(f32x4*)p = f32x4{a, b, c, d};
 }
 
+// Output epilogue through LDS.  In the accumulator layout lane l holds 64
+// values of query row l mod 32, so a direct store instruction writes 16
+// bytes into each of 32 rows.  Here the wavefront's 32 rows, normalised and
+// converted, go into a free LDS slice in row-major order (16-byte chunk c of
+// row r at chunk c ^ (r mod C), C chunks per row, conflict-free both ways)
+// and are read back so that each lane stores 16 contiguous bytes and a store
+// instruction covers whole rows.  The slice is this wavefront's own and
+// wavefront-local LDS accesses complete in order, so no barrier is needed.
+// out0 is row 0 of the wavefront's rows (rows sn elements apart); rows at or
+// past n_rows are not stored.
+template <int D, typename OutT>
+__device__ __forceinline__ void store_rows_staged(const f32x16 (&o)[D / 32], float inv,
+                                                  char* slice, OutT* out0, int sn, int n_rows,
+                                                  int lane) {
+  constexpr int kChunk = 16 / (int)sizeof(OutT);  // elements per 16-byte chunk
+  constexpr int C = D / kChunk;                   // chunks per row
+  constexpr int kRowBytes = D * (int)sizeof(OutT);
+  const int r = lane & 31;
+  const int half = lane >> 5;
+#pragma unroll
+  for (int dg = 0; dg < D / 32; ++dg)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      // elements d = 32 dg + 8 r4 + 4 half + 0..3 of row r
+      const float a = o[dg][4 * r4 + 0] * inv, b = o[dg][4 * r4 + 1] * inv;
+      const float c = o[dg][4 * r4 + 2] * inv, d = o[dg][4 * r4 + 3] * inv;
+      if constexpr (sizeof(OutT) == 2) {
+        const int ch = 4 * dg + r4;
+        *(SA_LDS bf16x4*)(slice + r * kRowBytes + ((ch ^ (r % C)) << 4) + 8 * half) =
+            bf16x4{(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+      } else {
+        const int ch = 8 * dg + 2 * r4 + half;
+        *(SA_LDS f32x4*)(slice + r * kRowBytes + ((ch ^ (r % C)) << 4)) = f32x4{a, b, c, d};
+      }
+    }
+  constexpr int kRowsPerStore = 64 / C;
+  const int cl = lane % C;
+  const int rl = lane / C;
+#pragma unroll
+  for (int j = 0; j < 32 / kRowsPerStore; ++j) {
+    const int row = j * kRowsPerStore + rl;
+    const u32x4 v = *(const SA_LDS u32x4*)(slice + row * kRowBytes + ((cl ^ (row % C)) << 4));
+    if (row < n_rows) *(u32x4*)(out0 + ((uint32_t)(row * sn) + (uint32_t)(cl * kChunk))) = v;
+  }
+}
+
+// The staged epilogue needs 32 D sizeof(OutT) bytes per wavefront out of the
+// item's K and V tiles (2 BK D bf16).
+template <int BQ, int BK, int D, typename OutT>
+constexpr bool kStagedStore = BQ * (int)sizeof(OutT) <= 4 * BK;
+
 // DENSE = true is the maskless path: every key block 0 .. n_kb - 1 is enabled
 // (counts, lists and order unused) and the items are laid out for the XCDs
 // as the schedule lays them out, with the (b, h) groups in index order.
@@ -385,7 +436,18 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
   const int l32_e = lane_e & 31;
   const int half_e = lane_e >> 5;
   const int row0 = u * BQ + wave_u * 32;  // first query row of this wavefront
-  if (row0 + l32_e < N) {
+  if constexpr (kStagedStore<BQ, BK, D, OutT>) {
+    // the loop's last barrier follows every wave's last LDS read, and no copy
+    // is outstanding: wavefront w stages its rows in bytes [w S, (w + 1) S)
+    // of [Ks | Vs], S = 32 D sizeof(OutT)
+    if (half_e == 0 && row0 + l32_e < N)
+      LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
+    constexpr int kSlice = 32 * D * (int)sizeof(OutT);
+    constexpr int kTileBytes = BK * D * 2;
+    const int off = wave_u * kSlice;
+    char* slice = off < kTileBytes ? (char*)Ks + off : (char*)Vs + (off - kTileBytes);
+    store_rows_staged<D, OutT>(o, inv, slice, O + base + (int64_t)row0 * sn, sn, N - row0, lane_e);
+  } else if (row0 + l32_e < N) {
     if (half_e == 0)
       LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
     OutT* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
@@ -628,7 +690,20 @@ __global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
   const int l32_e = lane_e & 31;
   const int half_e = lane_e >> 5;
   const int row0 = u * BQ + gwave_u * 32;
-  if (has_item && row0 + l32_e < N) {
+  if constexpr (kStagedStore<BQ, BK, D, OutT>) {
+    // every wavefront's LDS reads and copies are over (the last barrier
+    // above), so this item's K and V tiles are free: wavefront w of the item
+    // stages its rows in bytes [w S, (w + 1) S) of [Ks | Vs], S = 32 D sizeof(OutT)
+    if (has_item) {
+      if (half_e == 0 && row0 + l32_e < N)
+        LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
+      constexpr int kSlice = 32 * D * (int)sizeof(OutT);
+      constexpr int kTileBytes = BK * D * 2;
+      const int off = gwave_u * kSlice;
+      char* slice = off < kTileBytes ? (char*)Ks + off : (char*)Vs + (off - kTileBytes);
+      store_rows_staged<D, OutT>(o, inv, slice, O + base + (int64_t)row0 * sn, sn, N - row0, lane_e);
+    }
+  } else if (has_item && row0 + l32_e < N) {
     if (half_e == 0)
       LSE[(int64_t)bh * N + row0 + l32_e] = l_tot > 0.f ? (m_run + fast_log2(l_tot)) * kLn2 : -INFINITY;
     OutT* orow = (O + base + (int64_t)row0 * sn) + (uint32_t)(l32_e * sn);
