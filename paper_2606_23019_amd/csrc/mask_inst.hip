@@ -12,7 +12,7 @@
 // threshold loop.  The map is read from memory once per 16 thresholds (a
 // head's map serves every timestep of its layer; the re-reads hit in L2): 4
 // bytes read per block, one bit written per block and threshold, three vector
-// instructions per 64 bits.
+// instructions per 64 bits (the compare and two lane writes).
 
 #include "device_common.h"
 #include "launch.h"
@@ -22,8 +22,35 @@ namespace sa {
 namespace {
 
 constexpr int kInstWaves = 4;
+
 constexpr int kGroup = 8;     // words whose map entries a lane holds in registers at once
 constexpr int kInstThr = 16;  // thresholds per wavefront (grid.y splits larger sets)
+
+// lo and hi hold the two halves of a wavefront-uniform 64-bit word in lane K,
+// other lanes unchanged (v_writelane_b32).  The word is a ballot just written
+// by a vector compare, and a vector read of a vector-written scalar needs two
+// wait states first; one statement keeps the two writes behind the wait.
+template <int K>
+__device__ __forceinline__ void write_lane_k(uint32_t& lo, uint32_t& hi, uint64_t word) {
+  asm("s_nop 1\n\tv_writelane_b32 %0, %2, %4\n\tv_writelane_b32 %1, %3, %4"
+      : "+v"(lo), "+v"(hi)
+      : "s"((uint32_t)word), "s"((uint32_t)(word >> 32)), "n"(K));
+}
+// The same for a k < kGroup that is a constant once the caller's loop is
+// unrolled.
+static_assert(kGroup <= 8, "write_lane covers lanes 0..7");
+__device__ __forceinline__ void write_lane(uint32_t& lo, uint32_t& hi, uint64_t word, int k) {
+  switch (k) {
+    case 0: write_lane_k<0>(lo, hi, word); break;
+    case 1: write_lane_k<1>(lo, hi, word); break;
+    case 2: write_lane_k<2>(lo, hi, word); break;
+    case 3: write_lane_k<3>(lo, hi, word); break;
+    case 4: write_lane_k<4>(lo, hi, word); break;
+    case 5: write_lane_k<5>(lo, hi, word); break;
+    case 6: write_lane_k<6>(lo, hi, word); break;
+    default: write_lane_k<7>(lo, hi, word); break;
+  }
+}
 
 __global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
     const float* __restrict__ T, const float* __restrict__ p, int n_p, int H, int n_qb, int n_kb,
@@ -55,10 +82,7 @@ __global__ __launch_bounds__(64 * kInstWaves) void mask_inst_kernel(
       for (int k = 0; k < kGroup; ++k) {
         if (k < nw) {  // uniform
           const uint64_t word = __ballot(t[k] <= pi);
-          if (lane == k) {
-            lo = (uint32_t)word;
-            hi = (uint32_t)(word >> 32);
-          }
+          write_lane(lo, hi, word, k);
         }
       }
       if (lane < nw)
