@@ -64,11 +64,15 @@ __device__ __forceinline__ float pair_sum(float x) {
 // dispatcher deals workgroups round-robin), and each XCD takes its positions
 // in increasing order.  Given n_units groups of n_qb items, ranked 0 ..
 // n_units - 1, position pos = x + 8 j is item j of sequence x, where sequence
-// x holds chunk x of every group in rank order: a group's items are cut into 8
-// runs of consecutive u, run x holding q = n_qb / 8 items plus one when x is
-// one of (k r + i) mod 8, i < r = n_qb mod 8, for the group of rank k (the
-// leftovers rotate, so every sequence is exactly as long as its share of
-// positions).  Returns the rank k and writes the item's u.
+// x holds one chunk of every group in rank order.  The group of rank k gives
+// sequence x q = n_qb / 8 items plus one when x is one of (k r + i) mod 8,
+// i < r = n_qb mod 8 (the leftovers rotate, so every sequence is exactly as
+// long as its share of positions), and the chunks are runs of consecutive u:
+// sequence x takes the run at place (x + k) mod 8 in u order.  The rotation
+// spreads the first and last query blocks of each group (whose key windows
+// are cut short at the ends of the video) over all XCDs, so no XCD gets the
+// light end chunks of every group.  Returns the rank k and writes the
+// item's u.
 constexpr int kXcds = 8;  // accelerator complex dies of an MI355X, one L2 each
 
 // Items of sequence x in the groups of rank < k: k q plus the t < k r with
@@ -78,13 +82,16 @@ __device__ __forceinline__ int64_t xcd_prefix(int k, int x, int q, int r) {
   return (int64_t)k * q + (t > 0 ? (t + kXcds - 1) / kXcds : 0);
 }
 
-// First u of chunk x of the group of rank k: x q plus the sequences x' < x
-// that take one of this group's leftover items.
+// First u of sequence x's chunk of the group of rank k.  Its run is at
+// place p = (x + k) mod 8, so u0 is p q plus the runs before it that hold a
+// leftover item: the run at place p' belongs to sequence (p' - k) mod 8, which
+// has one when p' = (k (r + 1) + i) mod 8 for an i < r.
 __device__ __forceinline__ int xcd_chunk_u0(int k, int x, int q, int r) {
+  const int p = (x + k) % kXcds;
   int before = 0;
 #pragma unroll
-  for (int i = 0; i < kXcds - 1; ++i) before += (i < r && ((k * r + i) % kXcds) < x) ? 1 : 0;
-  return x * q + before;
+  for (int i = 0; i < kXcds - 1; ++i) before += (i < r && ((k * (r + 1) + i) % kXcds) < p) ? 1 : 0;
+  return p * q + before;
 }
 
 __device__ __forceinline__ int xcd_slice(int64_t pos, int n_units, int n_qb, int* u_out) {

@@ -14,18 +14,21 @@
 // started heaviest first, and the order is laid out for the 8 XCDs, each
 // with its own L2.  Workgroups are dealt to the XCDs round-robin (launch
 // position p runs on XCD p mod 8, in increasing p), so the order is written
-// as 8 interleaved sequences: sequence x holds chunk x of every group, the
+// as 8 interleaved sequences: sequence x holds one chunk of every group, the
 // groups heaviest first, where a group's n_qb query blocks are cut into 8
-// consecutive chunks of n_qb / 8 (the n_qb mod 8 leftover items rotate over
-// the XCDs from group to group, which makes every sequence exactly as long
-// as the positions p = x mod 8).  Each XCD thus works on a few groups at a
-// time, on neighbouring query blocks that share most key blocks in
+// runs of n_qb / 8 consecutive blocks (the n_qb mod 8 leftover items rotate
+// over the XCDs from group to group, which makes every sequence exactly as
+// long as the positions p = x mod 8) and sequence x takes the run at place
+// (x + k) mod 8 for the group of rank k.  Each XCD thus works on a few groups
+// at a time, on neighbouring query blocks that share most key blocks in
 // structured masks, so their K/V tiles are reused from its L2, and every XCD
-// gets an equal slice of every group, so the load stays balanced.  One
-// workgroup computes each group's total enabled blocks, ranks the groups in
-// LDS (by counting smaller keys, or with a bitonic network beyond 512 groups)
-// and writes the order, each chunk in ascending u; a second kernel then sorts every window of up to 64 places of
-// a chunk by enabled-block count, so that the items the attention kernel
+// gets an equal share of every group and, over the groups, of every part of
+// the sequence (the first and last query blocks of a video have fewer key
+// blocks), so the load stays balanced.  One workgroup computes each group's
+// total enabled blocks, ranks the groups in LDS (by counting smaller keys, or
+// with a bitonic network beyond 512 groups) and writes the order, each chunk
+// in ascending u; a second kernel then sorts every window of up to 64 places
+// of a chunk by enabled-block count, so that the items the attention kernel
 // runs side by side have similar counts.
 
 #include "device_common.h"

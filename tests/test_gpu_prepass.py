@@ -77,22 +77,28 @@ def test_prepass_ignores_bits_past_last_block():
 
 
 def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
-    """The documented order, built literally: sequence x gets chunk x of every
-    group (groups heaviest first), chunks of n_qb // 8 items plus one leftover
-    item for the sequences (k r + i) mod 8, i < r = n_qb mod 8, of the group of
-    rank k.  Each chunk is cut into windows of up to 64 consecutive query
-    blocks; the i-th window of a sequence holds its query blocks by decreasing
-    enabled-block count (ties by u) when i is even, the reverse when i is odd.
-    Position x + 8 j holds item j of sequence x.  row_counts[unit][u] is the
-    enabled-block count of query block u of group unit."""
+    """The documented order, built literally: sequence x gets one chunk of every
+    group (groups heaviest first).  The group of rank k gives sequence x
+    n_qb // 8 items plus one leftover item when x is one of (k r + i) mod 8,
+    i < r = n_qb mod 8, and its chunks are runs of consecutive query blocks,
+    sequence x taking the run at place (x + k) mod 8 in u order.  Each chunk is
+    cut into windows of up to 64 consecutive query blocks; the i-th window of
+    a sequence holds its query blocks by decreasing enabled-block count (ties
+    by u) when i is even, the reverse when i is odd.  Position x + 8 j holds
+    item j of sequence x.  row_counts[unit][u] is the enabled-block count of
+    query block u of group unit."""
     q, r = divmod(n_qb, xcds)
     seqs = [[] for _ in range(xcds)]
     n_win = [0] * xcds
     for k, unit in enumerate(units_sorted):
         extra = {(k * r + i) % xcds for i in range(r)}
-        start = 0
+        sizes = [q + (1 if x in extra else 0) for x in range(xcds)]
+        starts, at = {}, 0
+        for x in sorted(range(xcds), key=lambda x: (x + k) % xcds):  # runs in place order
+            starts[x] = at
+            at += sizes[x]
         for x in range(xcds):
-            size = q + (1 if x in extra else 0)
+            start, size = starts[x], sizes[x]
             for w0 in range(start, start + size, win):
                 us = sorted(range(w0, min(w0 + win, start + size)),
                             key=lambda u: (-row_counts[unit][u], u))
@@ -100,7 +106,6 @@ def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
                     us.reverse()
                 n_win[x] += 1
                 seqs[x].extend(unit * n_qb + u for u in us)
-            start += size
     order = [None] * (len(units_sorted) * n_qb)
     for x, seq in enumerate(seqs):
         for j, item in enumerate(seq):
