@@ -27,7 +27,8 @@
 //      gfx950 transposing read ds_read_b64_tr_b16.
 //
 // Epilogue: out = O / l rounded to bf16 (or kept in fp32 for the fp32-output
-// entry points), lse = (m + log2 l) ln 2.
+// entry points), lse = (m + log2 l) ln 2; the rows go out through the free
+// K/V tiles in LDS so that stores write whole rows (store_rows_staged).
 // The same kernels with DENSE = true are the maskless path (every key block).
 // Keys past N (ragged last block) are loaded as zeros and get -inf logits.
 
