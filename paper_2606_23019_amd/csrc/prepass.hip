@@ -192,7 +192,10 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
 // cut into windows of up to 64 places, and inside a window the query blocks
 // are placed by enabled-block count: decreasing in even windows of the
 // sequence, increasing in odd ones, so that a pair which straddles two
-// windows also meets counts from the same end.  The window still holds the
+// windows also meets counts from the same end, and decreasing in the
+// sequence's last window whatever its parity, so that every XCD ends its
+// work on its lightest items, which shortens the tail of the launch.  The
+// window still holds the
 // same consecutive query blocks, so the L2 reuse of their K/V tiles is
 // unchanged.  The places of window (x, k, wi) depend on k only, not on which
 // group has rank k, so this runs after schedule_kernel on the order it wrote,
@@ -239,11 +242,15 @@ __global__ __launch_bounds__(64 * kWindowSortWaves) void window_sort_kernel(
     rank += (kv[0] > key ? 1 : 0) + (kv[1] > key ? 1 : 0) + (kv[2] > key ? 1 : 0) +
             (kv[3] > key ? 1 : 0);
   }
-  // windows of sequence x before this one: chunks of q places have
-  // ceil(q / 64) windows, chunks of q + 1 one more when 64 divides q
-  const int64_t before = (int64_t)k * ((q + kSchedWindow - 1) / kSchedWindow) +
-                         (q % kSchedWindow == 0 ? j0 - (int64_t)k * q : 0) + wi;
-  const int t = (before & 1) ? L - 1 - rank : rank;
+  // windows of sequence x before this one and in all: chunks of q places
+  // have ceil(q / 64) windows, chunks of q + 1 one more when 64 divides q
+  const int per_q = (q + kSchedWindow - 1) / kSchedWindow;
+  const bool edge = q % kSchedWindow == 0;
+  const int64_t before = (int64_t)k * per_q + (edge ? j0 - (int64_t)k * q : 0) + wi;
+  const int64_t total = (int64_t)n_units * per_q +
+                        (edge ? xcd_prefix(n_units, x, q, r) - (int64_t)n_units * q : 0);
+  const bool increasing = (before & 1) && before != total - 1;
+  const int t = increasing ? L - 1 - rank : rank;
   if (lane < L) order[x + kXcds * (first + t)] = item;
 }
 

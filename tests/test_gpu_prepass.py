@@ -84,12 +84,12 @@ def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
     sequence x taking the run at place (x + k) mod 8 in u order.  Each chunk is
     cut into windows of up to 64 consecutive query blocks; the i-th window of
     a sequence holds its query blocks by decreasing enabled-block count (ties
-    by u) when i is even, the reverse when i is odd.  Position x + 8 j holds
-    item j of sequence x.  row_counts[unit][u] is the enabled-block count of
-    query block u of group unit."""
+    by u) when i is even or the window is the sequence's last, the reverse
+    otherwise.  Position x + 8 j holds item j of sequence x.
+    row_counts[unit][u] is the enabled-block count of query block u of group
+    unit."""
     q, r = divmod(n_qb, xcds)
-    seqs = [[] for _ in range(xcds)]
-    n_win = [0] * xcds
+    wins = [[] for _ in range(xcds)]  # each sequence's windows, sorted decreasing
     for k, unit in enumerate(units_sorted):
         extra = {(k * r + i) % xcds for i in range(r)}
         sizes = [q + (1 if x in extra else 0) for x in range(xcds)]
@@ -102,10 +102,12 @@ def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
             for w0 in range(start, start + size, win):
                 us = sorted(range(w0, min(w0 + win, start + size)),
                             key=lambda u: (-row_counts[unit][u], u))
-                if n_win[x] % 2:
-                    us.reverse()
-                n_win[x] += 1
-                seqs[x].extend(unit * n_qb + u for u in us)
+                wins[x].append([unit * n_qb + u for u in us])
+    seqs = [[] for _ in range(xcds)]
+    for x in range(xcds):
+        n = len(wins[x])
+        for i, wlist in enumerate(wins[x]):
+            seqs[x].extend(wlist[::-1] if i % 2 and i != n - 1 else wlist)
     order = [None] * (len(units_sorted) * n_qb)
     for x, seq in enumerate(seqs):
         for j, item in enumerate(seq):
