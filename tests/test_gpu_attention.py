@@ -285,6 +285,33 @@ def test_entry_points_agree_bitwise_and_runs_are_deterministic():
     plan.close()
 
 
+def test_back_to_back_one_shot_calls_match_the_prepared_path():
+    # The one-shot call enqueues pre-pass, schedule, window sort and attention
+    # on one stream; the attention kernel reads the order the window sort
+    # permutes in place.  Thirty calls in a row at 14B-480p, with no host
+    # synchronisation between them, must each equal the prepared path's bits.
+    torch = _torch()
+    from paper_2606_23019_amd import binding
+    wl = WAN14B_480P
+    packed, _, _ = masks_for(wl)
+    q, k, v = qkv_for(wl, device="cuda")
+    mask = binding.mask_to_device(packed)
+    counts, lists = binding.mask_prepass(mask, wl.H, wl.n_qb, wl.n_kb)
+    order = binding.schedule(counts, wl.B, wl.H, wl.n_qb)
+    ref_o, ref_l = binding.bsattn_fwd_prepared(q, k, v, counts, lists, order, wl.blk_q, wl.blk_k,
+                                               wl.scale)
+    out, lse = torch.empty_like(ref_o), torch.empty_like(ref_l)
+    bad = torch.zeros((), dtype=torch.int32, device="cuda")
+    for _ in range(30):
+        out.fill_(0.0)
+        binding.bsattn_fwd(q, k, v, mask, wl.blk_q, wl.blk_k, wl.scale, out=out, lse=lse)
+        bad += (~torch.eq(out.view(torch.int16), ref_o.view(torch.int16))).any().to(torch.int32)
+        bad += (~torch.eq(lse, ref_l)).any().to(torch.int32)
+    assert int(bad) == 0
+    del q, k, v, out, lse, ref_o, ref_l
+    torch.cuda.empty_cache()
+
+
 def test_invalid_arguments_write_nothing():
     torch = _torch()
     from paper_2606_23019_amd import binding
