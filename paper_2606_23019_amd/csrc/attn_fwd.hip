@@ -14,8 +14,9 @@
 //   1. the workgroup copies K[kb] and V[kb] (BK x D bf16, row-major) from
 //      global memory into LDS (16-byte chunks, XOR-swizzled per row);
 //   2. every wavefront computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16:
-//      Q^T (its 32 queries) stays in registers as the B operand, K rows come
-//      from LDS as the A operand.  In the transposed product each lane owns
+//      Q^T (its 32 queries) stays in registers as the B operand (read once
+//      per item, in the ping-pong kernel through LDS where the tiles are
+//      square), K rows come from LDS as the A operand.  In the transposed product each lane owns
 //      one query column, so the row statistics of the softmax are lane-local
 //      apart from one exchange between the two half-wavefronts;
 //   3. online softmax in fp32 in the log2 domain: running max m and sum l,
@@ -232,13 +233,24 @@ __device__ __forceinline__ void store_rows_staged(const f32x16 (&o)[D / 32], flo
       }
     }
   constexpr int kRowsPerStore = 64 / C;
+  constexpr int kStores = 32 / kRowsPerStore;
   const int cl = lane % C;
   const int rl = lane / C;
+  // All read-backs go out before the first store: the empty asm takes each
+  // value where it is read, so the reads are not sunk into the guarded
+  // stores below, where each would wait for its own LDS round trip.
+  u32x4 v[kStores];
 #pragma unroll
-  for (int j = 0; j < 32 / kRowsPerStore; ++j) {
+  for (int j = 0; j < kStores; ++j) {
     const int row = j * kRowsPerStore + rl;
-    const u32x4 v = *(const SA_LDS u32x4*)(slice + row * kRowBytes + ((cl ^ (row % C)) << 4));
-    if (row < n_rows) *(u32x4*)(out0 + ((uint32_t)(row * sn) + (uint32_t)(cl * kChunk))) = v;
+    v[j] = *(const SA_LDS u32x4*)(slice + row * kRowBytes + ((cl ^ (row % C)) << 4));
+  }
+#pragma unroll
+  for (int j = 0; j < kStores; ++j) asm volatile("" : "+v"(v[j]));
+#pragma unroll
+  for (int j = 0; j < kStores; ++j) {
+    const int row = j * kRowsPerStore + rl;
+    if (row < n_rows) *(u32x4*)(out0 + ((uint32_t)(row * sn) + (uint32_t)(cl * kChunk))) = v[j];
   }
 }
 
@@ -304,6 +316,8 @@ __global__ __launch_bounds__(BQ / 32 * 64, (kWavesPerSimd<BQ, BK, D>)) void bsat
   if (cnt > 0) issue_tile_copy<T, BK, D>(Ks, Kb, kblk(0) * BK, N, sn, wave_u, lane, cp);
 
   // Q^T fragments (B operand): lane holds Q[qrow][16 dc + 8 half .. +7].
+  // (Staging them through the V tile as the ping-pong kernel does measured
+  // 0.2-0.6 % slower here: two more barriers against 16 KB of Q per item.)
   const int qrow = u * BQ + wave * 32 + l32;
   bf16x8 qf[D / 16];
 #pragma unroll
@@ -578,14 +592,27 @@ __global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
   cp.init(gwave_u, lane, sn);
   if (cnt > 0) issue_tile_copy<T, BK, D>(Ks, Kb, first * BK, N, sn, gwave_u, lane, cp);
 
+  // Q^T fragments (B operand): lane holds Q[row gwave 32 + l32 of the item]
+  // [16 dc + 8 half .. +7].  With square tiles the item's Q rows come in as
+  // one more tile copy, into its V tile (free until the first softmax phase
+  // issues V[0]), and are read from there after the barriers below: rows of
+  // 256 contiguous bytes per four lanes instead of 32 rows per load
+  // instruction.  In a ragged last query block, rows past N hold row N - 1
+  // (their outputs are not stored); a workgroup slot without an item copies
+  // the clamped item's rows and stores nothing.
+  constexpr bool kStageQ = BQ == BK;
   const int qrow = u * BQ + gwave * 32 + l32;
   bf16x8 qf[D / 16];
+  if constexpr (kStageQ) {
+    issue_tile_copy<T, BK, D>(Vs, Qb, u * BQ, N, sn, gwave_u, lane, cp);
+  } else {
 #pragma unroll
-  for (int dc = 0; dc < D / 16; ++dc) {
-    if (has_item && qrow < N)
-      qf[dc] = *(const bf16x8*)(Qb + (int64_t)qrow * sn + dc * 16 + half * 8);
-    else
-      qf[dc] = bf16x8{};
+    for (int dc = 0; dc < D / 16; ++dc) {
+      if (has_item && qrow < N)
+        qf[dc] = *(const bf16x8*)(Qb + (int64_t)qrow * sn + dc * 16 + half * 8);
+      else
+        qf[dc] = bf16x8{};
+    }
   }
   __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): Q and K[0] landed
 
@@ -601,7 +628,16 @@ __global__ __launch_bounds__(512, 1) void bsattn_fwd_pp_kernel(
   for (int c = 0; c < BK / 16; ++c) pf[c] = bf16x8{};
 
   if (grp == 1) barrier_lds_reads_done();  // the second group runs one phase behind
-  barrier_lds_reads_done();                // both groups' K[0] tiles are in LDS
+  barrier_lds_reads_done();                // both groups' K[0] (and Q) tiles are in LDS
+  if constexpr (kStageQ) {
+    // every wavefront's Q copy landed before the first barrier; the group's
+    // reads complete before the barrier that ends its first MFMA phase,
+    // after which its first softmax phase reuses the tile for V[0]
+    const int qr = gwave * 32 + l32;
+#pragma unroll
+    for (int dc = 0; dc < D / 16; ++dc)
+      qf[dc] = lds_read_b128(Vs + qr * D + (((2 * dc + half) ^ swz<D>(qr)) << 3));
+  }
 
   for (int t = 0; t <= n_iter; ++t) {
     // ---- MFMA phase: P V of block t - 1, then S of block t
