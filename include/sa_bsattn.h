@@ -199,12 +199,14 @@ SA_API int sa_resize_threshold_map(const float* T, int H, int n_qb, int n_kb, fl
  * groups are ranked by decreasing total enabled blocks (ties by index).
  * With q = n_qb / 8 and r = n_qb mod 8, the group of rank k is cut into 8
  * chunks of consecutive u, chunk x holding q items plus one more when x is one
- * of (k r + i) mod 8, i < r.  Positions x, x + 8, x + 16, ... hold chunk x of
+ * of (k r + i) mod 8, i < r; in u order the chunks follow by place
+ * (x + k) mod 8.  Positions x, x + 8, x + 16, ... (sequence x) hold chunk x of
  * every group in rank order.  Each chunk is cut into windows of up to 64
- * consecutive u; the i-th window of a sequence holds its query blocks by
- * decreasing enabled-block count (ties by u) when i is even, increasing when
- * i is odd, so that neighbouring positions of a sequence, which the attention
- * kernel runs side by side, have similar counts.  counts: device int32
+ * consecutive u; the i-th window of a chunk holds its query blocks by
+ * decreasing enabled-block count (ties by u) when i is even or the window is
+ * the sequence's last, increasing otherwise, so that neighbouring positions
+ * of a sequence, which the attention kernel runs side by side, have similar
+ * counts.  counts: device int32
  * [H * n_qb] from the pre-pass (any values give a permutation).  order:
  * device int32 [B * H * n_qb].  With more than 4096 (b, h) groups the order
  * is the identity.

@@ -190,14 +190,18 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
 // kernel runs neighbouring places of a sequence side by side (two per
 // ping-pong workgroup, in lockstep over the larger count), so each chunk is
 // cut into windows of up to 64 places, and inside a window the query blocks
-// are placed by enabled-block count: decreasing in even windows of the
-// sequence, increasing in odd ones, so that a pair which straddles two
-// windows also meets counts from the same end, and decreasing in the
+// are placed by enabled-block count: decreasing in the even windows of the
+// chunk, increasing in its odd ones, so that a pair which straddles two
+// windows of a chunk meets counts from the same end, and decreasing in the
 // sequence's last window whatever its parity, so that every XCD ends its
-// work on its lightest items, which shortens the tail of the launch.  The
-// window still holds the
-// same consecutive query blocks, so the L2 reuse of their K/V tiles is
-// unchanged.  The places of window (x, k, wi) depend on k only, not on which
+// work on its lightest items, which shortens the tail of the launch.  Every
+// chunk thus starts on its heaviest items: while the light end of one group
+// finishes, the next group's long items start, and fewer groups' K/V tiles
+// compete for an XCD's L2 at a time than when every other chunk started light
+// (L2 fetches over the fabric per launch measured 20.4 against 23.9 GB at
+// 14B-480p, 5.3 against 8.2 GB at density 0.1 with structured masks; the
+// pair balance is the same).  A window still holds the same consecutive
+// query blocks.  The places of window (x, k, wi) depend on k only, not on which
 // group has rank k, so this runs after schedule_kernel on the order it wrote,
 // one wavefront per window across the whole chip: lane t reads the item at
 // the window's place t, keys it as (count << 6) | (63 - t) (distinct keys,
@@ -242,14 +246,10 @@ __global__ __launch_bounds__(64 * kWindowSortWaves) void window_sort_kernel(
     rank += (kv[0] > key ? 1 : 0) + (kv[1] > key ? 1 : 0) + (kv[2] > key ? 1 : 0) +
             (kv[3] > key ? 1 : 0);
   }
-  // windows of sequence x before this one and in all: chunks of q places
-  // have ceil(q / 64) windows, chunks of q + 1 one more when 64 divides q
-  const int per_q = (q + kSchedWindow - 1) / kSchedWindow;
-  const bool edge = q % kSchedWindow == 0;
-  const int64_t before = (int64_t)k * per_q + (edge ? j0 - (int64_t)k * q : 0) + wi;
-  const int64_t total = (int64_t)n_units * per_q +
-                        (edge ? xcd_prefix(n_units, x, q, r) - (int64_t)n_units * q : 0);
-  const bool increasing = (before & 1) && before != total - 1;
+  // direction: by the window's parity inside its chunk; the last window of
+  // the last chunk (the sequence's last) is decreasing
+  const bool last = k == n_units - 1 && (wi + 1) * kSchedWindow >= len;
+  const bool increasing = (wi & 1) && !last;
   const int t = increasing ? L - 1 - rank : rank;
   if (lane < L) order[x + kXcds * (first + t)] = item;
 }

@@ -83,8 +83,8 @@ def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
     i < r = n_qb mod 8, and its chunks are runs of consecutive query blocks,
     sequence x taking the run at place (x + k) mod 8 in u order.  Each chunk is
     cut into windows of up to 64 consecutive query blocks; the i-th window of
-    a sequence holds its query blocks by decreasing enabled-block count (ties
-    by u) when i is even or the window is the sequence's last, the reverse
+    a chunk holds its query blocks by decreasing enabled-block count (ties by
+    u) when i is even or the window is the sequence's last, the reverse
     otherwise.  Position x + 8 j holds item j of sequence x.
     row_counts[unit][u] is the enabled-block count of query block u of group
     unit."""
@@ -99,15 +99,15 @@ def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
             at += sizes[x]
         for x in range(xcds):
             start, size = starts[x], sizes[x]
-            for w0 in range(start, start + size, win):
+            for i, w0 in enumerate(range(start, start + size, win)):
                 us = sorted(range(w0, min(w0 + win, start + size)),
                             key=lambda u: (-row_counts[unit][u], u))
-                wins[x].append([unit * n_qb + u for u in us])
+                wins[x].append((i, [unit * n_qb + u for u in us]))
     seqs = [[] for _ in range(xcds)]
     for x in range(xcds):
         n = len(wins[x])
-        for i, wlist in enumerate(wins[x]):
-            seqs[x].extend(wlist[::-1] if i % 2 and i != n - 1 else wlist)
+        for j, (i, wlist) in enumerate(wins[x]):
+            seqs[x].extend(wlist[::-1] if i % 2 and j != n - 1 else wlist)
     order = [None] * (len(units_sorted) * n_qb)
     for x, seq in enumerate(seqs):
         for j, item in enumerate(seq):
