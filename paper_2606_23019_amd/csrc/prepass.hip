@@ -198,7 +198,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
 // chunk thus starts on its heaviest items: while the light end of one group
 // finishes, the next group's long items start, and fewer groups' K/V tiles
 // compete for an XCD's L2 at a time than when every other chunk started light
-// (L2 fetches over the fabric per launch measured 20.4 against 23.9 GB at
+// (L2 fetches over the fabric per launch measured 12.8 against 23.9 GB at
 // 14B-480p, 5.3 against 8.2 GB at density 0.1 with structured masks; the
 // pair balance is the same).  A window still holds the same consecutive
 // query blocks.  The places of window (x, k, wi) depend on k only, not on which
