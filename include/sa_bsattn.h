@@ -201,7 +201,7 @@ SA_API int sa_resize_threshold_map(const float* T, int H, int n_qb, int n_kb, fl
  * chunks of consecutive u, chunk x holding q items plus one more when x is one
  * of (k r + i) mod 8, i < r; in u order the chunks follow by place
  * (x + k) mod 8.  Positions x, x + 8, x + 16, ... (sequence x) hold chunk x of
- * every group in rank order.  Each chunk is cut into windows of up to 64
+ * every group in rank order.  Each chunk is cut into windows of up to 128
  * consecutive u; the i-th window of a chunk holds its query blocks by
  * decreasing enabled-block count (ties by u) when i is even or the window is
  * the sequence's last, increasing otherwise, so that neighbouring positions

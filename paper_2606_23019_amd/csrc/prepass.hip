@@ -27,7 +27,7 @@
 // blocks), so the load stays balanced.  One workgroup computes each group's
 // total enabled blocks, ranks the groups in LDS (by counting smaller keys, or
 // with a bitonic network beyond 512 groups) and writes the order, each chunk
-// in ascending u; a second kernel then sorts every window of up to 64 places
+// in ascending u; a second kernel then sorts every window of up to 128 places
 // of a chunk by enabled-block count, so that the items the attention kernel
 // runs side by side have similar counts.
 
@@ -77,7 +77,7 @@ __global__ __launch_bounds__(64 * kPrepassWaves) void prepass_kernel(
 
 constexpr int kSchedThreads = 1024;
 constexpr int kRankSortMax = 512;  // groups ranked by counting; more use the bitonic network
-constexpr int kSchedWindow = 64;  // one wavefront
+constexpr int kSchedWindow = 128;  // two places per lane of one wavefront
 
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* __restrict__ counts,
                                                                   int B, int H, int n_qb,
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
 // u0 .. u0 + len - 1 at sequence places prefix(k) .. + len - 1.  The attention
 // kernel runs neighbouring places of a sequence side by side (two per
 // ping-pong workgroup, in lockstep over the larger count), so each chunk is
-// cut into windows of up to 64 places, and inside a window the query blocks
+// cut into windows of up to 128 places, and inside a window the query blocks
 // are placed by enabled-block count: decreasing in the even windows of the
 // chunk, increasing in its odd ones, so that a pair which straddles two
 // windows of a chunk meets counts from the same end, and decreasing in the
@@ -203,11 +203,11 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(const int32_t* 
 // pair balance is the same).  A window still holds the same consecutive
 // query blocks.  The places of window (x, k, wi) depend on k only, not on which
 // group has rank k, so this runs after schedule_kernel on the order it wrote,
-// one wavefront per window across the whole chip: lane t reads the item at
-// the window's place t, keys it as (count << 6) | (63 - t) (distinct keys,
-// larger for larger counts and, among equal counts, for smaller t), counts
-// the larger keys of the window from a key row in LDS, and writes the item
-// back at its rank's place.  Each window's places are read and written by its
+// one wavefront per window across the whole chip: lane l reads the items at
+// the window's places t = l and l + 64, keys each as (count << 7) | (127 - t)
+// (distinct keys, larger for larger counts and, among equal counts, for
+// smaller t), counts the larger keys of the window from a key row in LDS, and
+// writes each item back at its rank's place.  Each window's places are read and written by its
 // own wavefront only, so the permutation happens in place.
 constexpr int kWindowSortWaves = 4;
 
@@ -230,28 +230,40 @@ __global__ __launch_bounds__(64 * kWindowSortWaves) void window_sort_kernel(
   const int L = min(kSchedWindow, len - wi * kSchedWindow);
   if (L <= 0) return;  // uniform per wavefront
   const int64_t first = j0 + (int64_t)wi * kSchedWindow;  // the window's first place
-  int item = 0, key = -1;  // lanes past the window hold -1, below every key
-  if (lane < L) {
-    item = order[x + kXcds * (first + lane)];
-    const int64_t row = (int64_t)(item / n_qb % H) * n_qb + item % n_qb;
-    key = (min(max(counts[row], 0), (1 << 24) - 1) << 6) | (63 - lane);
+  // lane l holds places l and l + 64 of the window; places past L hold -1,
+  // below every key
+  int item[2] = {0, 0}, key[2] = {-1, -1};
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int t = lane + 64 * h;
+    if (t < L) {
+      item[h] = order[x + kXcds * (first + t)];
+      const int64_t row = (int64_t)(item[h] / n_qb % H) * n_qb + item[h] % n_qb;
+      key[h] = (min(max(counts[row], 0), (1 << 23) - 1) << 7) | (127 - t);
+    }
   }
   int32_t* key_row = key_rows[wave];
-  key_row[lane] = key;
+  key_row[lane] = key[0];
+  key_row[lane + 64] = key[1];
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the wavefront's keys are in LDS
-  int rank = 0;  // window members placed before this one
+  int rank[2] = {0, 0};  // window members placed before each of the lane's two
 #pragma unroll 4
   for (int i = 0; i < L; i += 4) {  // keys past L (up to a multiple of 4) are -1
     const i32x4 kv = *(const SA_LDS i32x4*)(key_row + i);
-    rank += (kv[0] > key ? 1 : 0) + (kv[1] > key ? 1 : 0) + (kv[2] > key ? 1 : 0) +
-            (kv[3] > key ? 1 : 0);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      rank[h] += (kv[0] > key[h] ? 1 : 0) + (kv[1] > key[h] ? 1 : 0) +
+                 (kv[2] > key[h] ? 1 : 0) + (kv[3] > key[h] ? 1 : 0);
   }
   // direction: by the window's parity inside its chunk; the last window of
   // the last chunk (the sequence's last) is decreasing
   const bool last = k == n_units - 1 && (wi + 1) * kSchedWindow >= len;
   const bool increasing = (wi & 1) && !last;
-  const int t = increasing ? L - 1 - rank : rank;
-  if (lane < L) order[x + kXcds * (first + t)] = item;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int t = increasing ? L - 1 - rank[h] : rank[h];
+    if (lane + 64 * h < L) order[x + kXcds * (first + t)] = item[h];
+  }
 }
 
 }  // namespace

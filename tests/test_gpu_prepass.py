@@ -76,13 +76,13 @@ def test_prepass_ignores_bits_past_last_block():
         assert np.array_equal(a[r, :n[r]], b[r, :n[r]])
 
 
-def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=64):
+def _xcd_order(units_sorted, n_qb, row_counts, xcds=8, win=128):
     """The documented order, built literally: sequence x gets one chunk of every
     group (groups heaviest first).  The group of rank k gives sequence x
     n_qb // 8 items plus one leftover item when x is one of (k r + i) mod 8,
     i < r = n_qb mod 8, and its chunks are runs of consecutive query blocks,
     sequence x taking the run at place (x + k) mod 8 in u order.  Each chunk is
-    cut into windows of up to 64 consecutive query blocks; the i-th window of
+    cut into windows of up to 128 consecutive query blocks; the i-th window of
     a chunk holds its query blocks by decreasing enabled-block count (ties by
     u) when i is even or the window is the sequence's last, the reverse
     otherwise.  Position x + 8 j holds item j of sequence x.
