@@ -403,6 +403,27 @@ def test_bnhd_layout_matches_bhnd_bitwise(B, H, N, d, bq, bk, p, seed):
     assert torch.equal(o2.transpose(1, 2), o1) and torch.equal(l2, l1)
 
 
+def test_bnhd_layout_matches_bhnd_bitwise_at_14b_480p():
+    """The Wan-native [B, N, H, d] layout at the benchmark shape (row stride
+    H d = 5120 elements between a head's tokens) gives the same bits as the
+    [B, H, N, d] call."""
+    torch = _torch()
+    from paper_2606_23019_amd import binding
+    from workloads import configs, masks_for, qkv_for
+    wl = configs.SHORT["14b-480p"]
+    packed, _, _ = masks_for(wl)
+    q, k, v = qkv_for(wl, device="cuda")
+    o1, l1 = binding.bsattn_fwd(q, k, v, packed, wl.blk_q, wl.blk_k, wl.scale)
+    qt, kt, vt = (x.transpose(1, 2).contiguous() for x in (q, k, v))
+    del q, k, v
+    o2, l2 = binding.bsattn_fwd_bnhd(qt, kt, vt, packed, wl.blk_q, wl.blk_k, wl.scale)
+    torch.cuda.synchronize()
+    assert o2.shape == (wl.B, wl.N, wl.H, wl.d)
+    assert torch.equal(o2.transpose(1, 2), o1) and torch.equal(l2, l1)
+    del qt, kt, vt, o1, o2
+    torch.cuda.empty_cache()
+
+
 def test_bnhd_layout_parity_vs_reference():
     torch = _torch()
     from paper_2606_23019_amd import binding
